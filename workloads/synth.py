@@ -1,0 +1,348 @@
+"""Seeded synthetic workloads shaped like the paper's decode experiments.
+
+The paper's kernel workload (Experiments, microkernel evaluation) is batch
+decoding with h=32 heads, head dim d=128, chunk size c=64 and FP16 tensors,
+where every sequence starts with n_s shared prompt tokens. Real shared prompts
+(the system prompts of Table 2 and Appendix A) are not available here; random
+token ids of the same lengths stand in for them, and K/V/q are N(0,1) draws.
+
+Recipe (identical for every consumer):
+  * generator ``numpy.random.Generator(PCG64(1000 + config))``;
+  * draw order: prompt/branch tokens, per-sequence unique tokens, then K and V
+    once per segment (each shared prompt or branch once, each unique suffix
+    once), then q;
+  * values are drawn as float32 N(0,1) and rounded to the config dtype
+    (round-to-nearest-even); the rounded values are the ground truth;
+  * token ids are uniform in [0, 32000); the first token of a segment that
+    starts a new branch is redrawn until it differs from the first tokens of
+    its siblings, so the designed tree shape holds (``redraws`` counts them).
+
+Nothing here builds a tree or computes attention.
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import Iterator
+
+import numpy as np
+
+VOCAB = 32000
+
+CONFIG_NAMES = {
+    1: "tiny_p128_u32_b4_h2_d64_c16_fp32",
+    2: "single_prompt_p1024_u512_b32_h32_d128_c64_fp16",
+    3: "long_prompt_p4096_u512_b32_h32_d128_c64_fp16",
+    4: "multi_prompt_2level_b64_h32_d128_c64_fp16",
+    5: "dynamic_p2048_u64to1024_b128_h32_d128_c64_fp16_64steps",
+}
+
+
+@dataclasses.dataclass
+class Segment:
+    """A run of tokens with their K/V rows, [L], [L, H, d], [L, H, d]."""
+
+    tokens: np.ndarray
+    k: np.ndarray
+    v: np.ndarray
+
+    def __len__(self) -> int:
+        return int(self.tokens.shape[0])
+
+
+@dataclasses.dataclass
+class Sequence:
+    seq_id: int
+    segs: list  # indices into the workload's segment list, root first
+
+    def tokens(self, segments) -> np.ndarray:
+        return np.concatenate([segments[s].tokens for s in self.segs])
+
+    def kv(self, segments):
+        k = np.concatenate([segments[s].k for s in self.segs], axis=0)
+        v = np.concatenate([segments[s].v for s in self.segs], axis=0)
+        return k, v
+
+    def length(self, segments) -> int:
+        return sum(len(segments[s]) for s in self.segs)
+
+
+@dataclasses.dataclass
+class StaticWorkload:
+    config: int
+    name: str
+    H: int
+    d: int
+    c: int
+    dtype: np.dtype
+    scale: float
+    segments: list
+    seqs: list          # insert order; seq_id = position
+    q: np.ndarray       # [B, H, d], indexed by seq_id
+    redraws: int = 0
+
+    @property
+    def B(self) -> int:
+        return len(self.seqs)
+
+
+@dataclasses.dataclass
+class ChurnEvent:
+    removed: list       # seq ids removed (before the step's append)
+    added: list         # Sequence objects inserted afterwards
+    new_segments: dict  # segment index -> Segment for the added suffixes
+
+
+@dataclasses.dataclass
+class DecodeStep:
+    step: int
+    churn: ChurnEvent | None
+    live: np.ndarray    # sorted live seq ids after churn, int64 [n]
+    tokens: np.ndarray  # appended token per live seq, int32 [n]
+    k: np.ndarray       # appended K rows [n, H, d]
+    v: np.ndarray       # appended V rows [n, H, d]
+    q: np.ndarray       # queries [n, H, d] in live (sorted id) order
+
+
+@dataclasses.dataclass
+class DynamicWorkload:
+    """Config 5: initial tree plus a generator of decode steps."""
+
+    config: int
+    name: str
+    H: int
+    d: int
+    c: int
+    dtype: np.dtype
+    scale: float
+    segments: list          # grows as churn adds suffixes
+    seqs: list              # initial sequences, insert order
+    n_steps: int
+    churn_steps: tuple
+    churn_count: int
+    rng: np.random.Generator
+    redraws: int = 0
+
+    def steps(self) -> Iterator[DecodeStep]:
+        """Yield the decode steps in order; each draw follows the previous."""
+        rng = self.rng
+        live = {s.seq_id: s for s in self.seqs}
+        # first token of each live sequence's unique suffix (branch siblings)
+        first = {s.seq_id: int(self.segments[s.segs[-1]].tokens[0]) for s in self.seqs}
+        next_id = max(live) + 1
+        prompt_seg = self.seqs[0].segs[0]
+        for step in range(self.n_steps):
+            churn = None
+            if step in self.churn_steps:
+                ids = np.array(sorted(live), dtype=np.int64)
+                removed = sorted(int(x) for x in rng.choice(ids, size=self.churn_count, replace=False))
+                for r in removed:
+                    del live[r]
+                    del first[r]
+                lens = rng.integers(64, 1025, size=self.churn_count)
+                added, new_segments = [], {}
+                toks = []
+                for L in lens:
+                    t, nr = _draw_tokens(rng, int(L), set(first.values()))
+                    self.redraws += nr
+                    first[next_id] = int(t[0])
+                    toks.append((next_id, t))
+                    next_id += 1
+                for sid, t in toks:
+                    k = _draw_values(rng, (len(t), self.H, self.d), self.dtype)
+                    v = _draw_values(rng, (len(t), self.H, self.d), self.dtype)
+                    idx = len(self.segments)
+                    seg = Segment(t, k, v)
+                    self.segments.append(seg)
+                    new_segments[idx] = seg
+                    s = Sequence(sid, [prompt_seg, idx])
+                    added.append(s)
+                    live[sid] = s
+                churn = ChurnEvent(removed, added, new_segments)
+            ids = np.array(sorted(live), dtype=np.int64)
+            n = ids.shape[0]
+            tokens = rng.integers(0, VOCAB, size=n).astype(np.int32)
+            k = _draw_values(rng, (n, self.H, self.d), self.dtype)
+            v = _draw_values(rng, (n, self.H, self.d), self.dtype)
+            q = _draw_values(rng, (n, self.H, self.d), self.dtype)
+            yield DecodeStep(step, churn, ids, tokens, k, v, q)
+
+
+def _draw_tokens(rng, n, forbidden_first):
+    t = rng.integers(0, VOCAB, size=n).astype(np.int32)
+    redraws = 0
+    while int(t[0]) in forbidden_first:
+        t[0] = np.int32(rng.integers(0, VOCAB))
+        redraws += 1
+    return t, redraws
+
+
+def _draw_values(rng, shape, dtype):
+    return rng.standard_normal(size=shape, dtype=np.float32).astype(dtype)
+
+
+def _spec(config):
+    if config == 1:
+        return dict(H=2, d=64, c=16, dtype=np.dtype(np.float32))
+    if config in (2, 3, 4, 5):
+        return dict(H=32, d=128, c=64, dtype=np.dtype(np.float16))
+    raise ValueError(f"unknown config {config}")
+
+
+def make_static(config: int) -> StaticWorkload:
+    """Configs 1-4: a tree built once and one decode step of queries."""
+    sp = _spec(config)
+    H, d, c, dt = sp["H"], sp["d"], sp["c"], sp["dtype"]
+    rng = np.random.Generator(np.random.PCG64(1000 + config))
+    redraws = 0
+    seg_tokens = []   # token arrays in segment order
+    seqs = []
+    if config in (1, 2, 3):
+        P, U, B = {1: (128, 32, 4), 2: (1024, 512, 32), 3: (4096, 512, 32)}[config]
+        prompt, nr = _draw_tokens(rng, P, set())
+        redraws += nr
+        seg_tokens.append(prompt)
+        firsts = set()
+        for i in range(B):
+            t, nr = _draw_tokens(rng, U, firsts)
+            redraws += nr
+            firsts.add(int(t[0]))
+            seg_tokens.append(t)
+            seqs.append(Sequence(i, [0, 1 + i]))
+    else:  # config 4: two roots, two branches under each, 16 suffixes per branch
+        roots = []
+        rf = set()
+        for _ in range(2):
+            t, nr = _draw_tokens(rng, 1024, rf)
+            redraws += nr
+            rf.add(int(t[0]))
+            roots.append(len(seg_tokens))
+            seg_tokens.append(t)
+        branches = []
+        for r in roots:
+            bf = set()
+            for _ in range(2):
+                t, nr = _draw_tokens(rng, 1024, bf)
+                redraws += nr
+                bf.add(int(t[0]))
+                branches.append((r, len(seg_tokens)))
+                seg_tokens.append(t)
+        sid = 0
+        for r, b in branches:
+            sf = set()
+            for _ in range(16):
+                t, nr = _draw_tokens(rng, 256, sf)
+                redraws += nr
+                sf.add(int(t[0]))
+                seqs.append(Sequence(sid, [r, b, len(seg_tokens)]))
+                seg_tokens.append(t)
+                sid += 1
+    segments = []
+    for t in seg_tokens:
+        k = _draw_values(rng, (len(t), H, d), dt)
+        v = _draw_values(rng, (len(t), H, d), dt)
+        segments.append(Segment(t, k, v))
+    q = _draw_values(rng, (len(seqs), H, d), dt)
+    return StaticWorkload(config, CONFIG_NAMES[config], H, d, c, dt, 1.0 / np.sqrt(d),
+                          segments, seqs, q, redraws)
+
+
+def make_dynamic(config: int = 5, n_steps: int = 64, B: int = 128,
+                 prompt_len: int = 2048, H: int | None = None, d: int | None = None) -> DynamicWorkload:
+    """Config 5: shared prompt plus suffixes of U[64,1024] tokens, then decode.
+
+    Churn: before steps 16, 32 and 48, round(0.1*B) live sequences chosen
+    uniformly without replacement leave, and as many new ones (the same prompt
+    plus a fresh suffix) join with ids counting up from B.
+    ``H``/``d``/``B``/``prompt_len`` may be shrunk for fast tests; the draw
+    order is unchanged.
+    """
+    sp = _spec(config)
+    H = sp["H"] if H is None else H
+    d = sp["d"] if d is None else d
+    c, dt = sp["c"], sp["dtype"]
+    rng = np.random.Generator(np.random.PCG64(1000 + config))
+    redraws = 0
+    prompt, nr = _draw_tokens(rng, prompt_len, set())
+    redraws += nr
+    lens = rng.integers(64, 1025, size=B)
+    seg_tokens = [prompt]
+    firsts = set()
+    seqs = []
+    for i in range(B):
+        t, nr = _draw_tokens(rng, int(lens[i]), firsts)
+        redraws += nr
+        firsts.add(int(t[0]))
+        seg_tokens.append(t)
+        seqs.append(Sequence(i, [0, 1 + i]))
+    segments = []
+    for t in seg_tokens:
+        k = _draw_values(rng, (len(t), H, d), dt)
+        v = _draw_values(rng, (len(t), H, d), dt)
+        segments.append(Segment(t, k, v))
+    churn_steps = tuple(s for s in (16, 32, 48) if s < n_steps)
+    return DynamicWorkload(config, CONFIG_NAMES[config], H, d, c, dt, 1.0 / np.sqrt(d),
+                           segments, seqs, n_steps, churn_steps, int(round(0.1 * B)), rng, redraws)
+
+
+# ---------------------------------------------------------------------------
+# Random operation scripts for tree tests (small alphabets force sharing,
+# splits, sibling collisions and prefix sequences).
+
+def random_op_script(seed: int, n_ops: int = 40, alphabet: int = 3, max_len: int = 12,
+                     max_live: int = 8, p_insert: float = 0.35, p_extend: float = 0.2,
+                     p_append: float = 0.25):
+    """Return a list of operations (tuples) over live sequence ids.
+
+    ("insert", sid, tokens) | ("extend", sid, tokens) |
+    ("append", [sids], tokens[n]) | ("remove", sid)
+    Only ids are tracked here; the tree semantics live elsewhere.
+    """
+    rng = np.random.Generator(np.random.PCG64(seed))
+    ops = []
+    live = []
+    next_id = 0
+    for _ in range(n_ops):
+        u = rng.random()
+        if not live or (u < p_insert and len(live) < max_live):
+            n = int(rng.integers(1, max_len + 1))
+            t = rng.integers(0, alphabet, size=n).astype(np.int32)
+            ops.append(("insert", next_id, t))
+            live.append(next_id)
+            next_id += 1
+        elif u < p_insert + p_extend:
+            sid = int(live[int(rng.integers(0, len(live)))])
+            n = int(rng.integers(1, max_len // 2 + 2))
+            t = rng.integers(0, alphabet, size=n).astype(np.int32)
+            ops.append(("extend", sid, t))
+        elif u < p_insert + p_extend + p_append:
+            k = int(rng.integers(1, len(live) + 1))
+            sids = sorted(int(x) for x in rng.choice(np.array(live), size=k, replace=False))
+            t = rng.integers(0, alphabet, size=k).astype(np.int32)
+            ops.append(("append", sids, t))
+        else:
+            sid = int(live[int(rng.integers(0, len(live)))])
+            ops.append(("remove", sid))
+            live.remove(sid)
+    return ops
+
+
+def prefix_keyed_kv(seed: int, tokens: np.ndarray, start: int, H: int, d: int, dtype):
+    """K/V rows [start, n) where row i depends only on (seed, tokens[:i+1]).
+
+    Two sequences with a common token prefix then carry identical K/V for it,
+    which is what a prefix-shared cache assumes.
+    """
+    n = int(tokens.shape[0])
+    k = np.empty((n - start, H, d), dtype=dtype)
+    v = np.empty((n - start, H, d), dtype=dtype)
+    h = np.uint64(1469598103934665603)
+    prime = np.uint64(1099511628211)
+    with np.errstate(over="ignore"):
+        for i in range(n):
+            h = np.uint64((h ^ np.uint64(int(tokens[i]) & 0xFFFFFFFF)) * prime)
+            if i >= start:
+                g = np.random.Generator(np.random.PCG64([seed, int(h), i]))
+                x = g.standard_normal(size=(2, H, d), dtype=np.float32).astype(dtype)
+                k[i - start] = x[0]
+                v[i - start] = x[1]
+    return k, v
