@@ -1,0 +1,204 @@
+/*
+ * chunkattn.h - C ABI of an MI355X (gfx950) library for decode-phase
+ * self-attention over a prefix-aware, chunked KV cache, computed with the
+ * two-phase partition of ChunkAttention (arXiv 2402.15220).
+ *
+ * Paper passages the calls follow:
+ *   - Section 3.1 (PAKV): the KV cache is a forest of chunks, each holding at
+ *     most c tokens and the K and V slices of those tokens; a joining sequence
+ *     inserts a path (with prefix lookup), a leaving sequence deletes its
+ *     path, and decoding appends one token per sequence, growing a new chunk
+ *     when the leaf chunk is full; chunks come from a pool with a free list.
+ *   - Section 3.2 (TPP): attention for the last token of every live sequence,
+ *     Q in R^{b x d} per head (Algorithms 1 and 2, Eqn 1 and Eqn 2).
+ *   - Section 3.3: the kernel context (chunk, first and last covered query
+ *     row) is generated from the tree on the host and copied to the device
+ *     lazily, only when the tree structure changes.
+ *   - Section 3.2, prefill: a prefix lookup reports how many leading tokens
+ *     are already cached so their K/V need not be recomputed.
+ *
+ * Conventions for every call:
+ *   - Return value: CA_OK (0) or a negative ca_status. On failure nothing
+ *     observable changes (tree, tables, pool contents and slot ownership stay
+ *     as they were) and ca_last_error() returns a message for this thread.
+ *   - A cache is not thread-safe. All device work of a cache is enqueued on
+ *     the hipStream_t passed to the call; callers must use one stream per
+ *     cache, which also makes slot reuse after ca_remove safe (later writes
+ *     are stream-ordered after earlier reads).
+ *   - "host" pointers are read synchronously before the call returns;
+ *     "device" pointers must stay valid until the enqueued work completes.
+ *   - Tree row order: the query rows q and output rows o are ordered as the
+ *     sequences appear in a depth-first walk of the tree (children by
+ *     ascending first token; sequences that end at a node, by ascending id,
+ *     before that node's children). ca_seq_order() returns that order. The
+ *     rows covered by any chunk are then contiguous (Section 3.1).
+ */
+#ifndef CHUNKATTN_H
+#define CHUNKATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ca_cache ca_cache; /* opaque, owned by the library */
+
+typedef enum {
+  CA_OK = 0,
+  CA_ERR_INVALID = -1,   /* bad argument: null pointer, n < 1, negative token, bad shape */
+  CA_ERR_NOMEM = -2,     /* the chunk pool cannot supply the slots the call needs */
+  CA_ERR_NOT_FOUND = -3, /* unknown sequence id */
+  CA_ERR_EXISTS = -4,    /* sequence id already live */
+  CA_ERR_DEVICE = -5,    /* a HIP call failed; message holds hipGetErrorString */
+  CA_ERR_WORKSPACE = -6  /* workspace null or smaller than ca_workspace_size */
+} ca_status;
+
+typedef enum { CA_FP16 = 0, CA_FP32 = 1 } ca_dtype;
+
+/*
+ * Cache configuration (Section 3.1: chunk size c; the experiments use h=32,
+ * d=128, c=64, FP16).
+ *   chunk_size  c >= 1 tokens per chunk
+ *   num_heads   H >= 1
+ *   head_dim    d in {64, 128}
+ *   dtype       element type of K, V, q and o
+ *   num_slots   number of chunk slots in each pool (>= 1)
+ *   k_pool, v_pool  caller-owned device buffers, each at least
+ *               num_slots * H * c * d * sizeof(dtype) bytes, 16-byte aligned,
+ *               layout [slot][head][c][d] (row-major). The library writes
+ *               only rows it owns and never frees them.
+ *               Both NULL: a table-only cache that keeps the tree and its
+ *               tables but stores no K/V (k/v arguments must then be NULL and
+ *               ca_attention is refused). Used to exercise the host tree
+ *               without a GPU.
+ */
+typedef struct {
+  int32_t chunk_size;
+  int32_t num_heads;
+  int32_t head_dim;
+  ca_dtype dtype;
+  int64_t num_slots;
+  void* k_pool;
+  void* v_pool;
+} ca_config;
+
+/*
+ * Host views of the canonical kernel-context tables (Section 3.3, Figure 2;
+ * ranges are half-open [begin, end), Figure 2 prints the end inclusively).
+ * Node index = breadth-first level order, children by ascending first token.
+ *   row_seq[B]          sequence id of each query row
+ *   node_*[n_nodes]     slot, token count, covered rows [row_begin,row_end),
+ *                       parent node (-1 for a tree root), start position of
+ *                       the node's first token within its sequences
+ *   shr_node[n_shared]  nodes covered by >= 2 rows (Algorithm 1's chunks)
+ *   shr_part_base[n_shared]  running sum of their row counts: partial result
+ *                       (node, row r) has index shr_part_base + r - row_begin
+ *   priv_ptr[B+1], priv_node[]  per row, private nodes root -> leaf
+ *                       (Algorithm 2's chunks C_{k+1..l})
+ *   shr_ptr[B+1],  shr_part[]   per row, partial indices of its shared nodes,
+ *                       root -> leaf (Algorithm 2's partials C_1..C_k)
+ * Arrays are owned by the cache and valid until its next mutating call.
+ */
+typedef struct {
+  int64_t B, n_nodes, n_shared;
+  const int64_t* row_seq;
+  const int32_t *node_slot, *node_len, *node_row_begin, *node_row_end, *node_parent,
+      *node_start_pos;
+  const int32_t *shr_node, *shr_part_base;
+  const int32_t *priv_ptr, *priv_node, *shr_ptr, *shr_part;
+} ca_tables;
+
+/* Create a cache (Section 3.1). No device work; a HIP cache allocates its
+ * small device tables (slot lengths, work lists) on the current device.
+ * Errors: INVALID (c < 1, H < 1, d not 64/128, bad dtype, num_slots < 1, only
+ * one of the pools given), DEVICE. *out receives the handle. */
+ca_status ca_create(const ca_config* cfg, ca_cache** out);
+
+/* Destroy; NULL is accepted. Never frees the caller's pools. Synchronises
+ * nothing: the caller must have finished the cache's stream work. */
+ca_status ca_destroy(ca_cache* cache);
+
+/* Prefix lookup (Section 3.2, prefill): number of leading tokens of
+ * tokens[0..n) already present in the tree. tokens: host int32, n >= 1,
+ * every token >= 0. No mutation. */
+ca_status ca_match(const ca_cache* cache, const int32_t* tokens, int64_t n, int64_t* matched);
+
+/* A new sequence joins (Section 3.1): search the tree and insert its path.
+ * A fully matched chunk is descended; a mismatch or the end of the sequence
+ * inside a chunk splits that chunk (its tail moves to a fresh slot with its
+ * K/V rows copied); the remaining tokens become new chunks of at most c
+ * tokens. Spare room of a chunk that other sequences use is never filled.
+ *   tokens  host int32 [n], n >= 1, each >= 0
+ *   k, v    device [n][H][d] of dtype; rows < *matched are not read
+ *           (NULL for a table-only cache)
+ *   stream  hipStream_t for the K/V copies
+ *   matched nullable out: tokens already present
+ * Errors: INVALID, EXISTS, NOMEM (checked before any change), DEVICE. */
+ca_status ca_insert(ca_cache* cache, int64_t seq_id, const int32_t* tokens, int64_t n,
+                    const void* k, const void* v, void* stream, int64_t* matched);
+
+/* Extend a live sequence by n >= 1 tokens (Section 3.1, decoding). If its
+ * last chunk is used by it alone, that chunk is filled up to c first;
+ * otherwise the tokens are matched below the last chunk as in ca_insert.
+ * k, v: device [n][H][d]; rows < *matched are not read. Errors as ca_insert
+ * plus NOT_FOUND. */
+ca_status ca_extend(ca_cache* cache, int64_t seq_id, const int32_t* tokens, int64_t n,
+                    const void* k, const void* v, void* stream, int64_t* matched);
+
+/* One decode step: append tokens[i] to sequence seq_ids[i] for i < n_seqs,
+ * in the listed order (Section 3.1: append into leaf chunks, grow a chunk
+ * when full). seq_ids, tokens: host; k, v: device [n_seqs][H][d]. All or
+ * nothing: NOMEM leaves every sequence unchanged. Ids must be distinct. */
+ca_status ca_append_batch(ca_cache* cache, int64_t n_seqs, const int64_t* seq_ids,
+                          const int32_t* tokens, const void* k, const void* v, void* stream);
+
+/* A completed sequence leaves (Section 3.1): delete its path; chunks no
+ * longer used by any sequence return to the pool (freed leaf first, reused
+ * last-freed first). Chains are not merged. */
+ca_status ca_remove(ca_cache* cache, int64_t seq_id);
+
+/* Number of live sequences (B, the query rows of the next attention). */
+ca_status ca_num_seqs(const ca_cache* cache, int64_t* B);
+
+/* Tree row order: seq_ids[r] = id of the sequence whose query is row r.
+ * seq_ids: host int64 with room for cap >= B entries. */
+ca_status ca_seq_order(const ca_cache* cache, int64_t* seq_ids, int64_t cap);
+
+/* Bytes of device workspace ca_attention needs for the current tree
+ * (partial results of Algorithm 1 plus split partials; 0 is possible). */
+ca_status ca_workspace_size(const ca_cache* cache, size_t* bytes);
+
+/* Decode attention for every live sequence (Section 3.2, Algorithms 1 and 2):
+ * chunk-first partial attention (Eqn 1) over chunks shared by >= 2 rows with
+ * the covered query rows batched, sequence-first partial attention over each
+ * row's own chunks, online-softmax merge (Eqn 2) and O/n.
+ *   q      device [B][H][d] of dtype, tree row order (ca_seq_order)
+ *   o      device [B][H][d] of dtype, written in the same order
+ *   scale  softmax scale applied to q.k; 0 means 1/sqrt(d)
+ *   ws     device workspace of ws_bytes >= ca_workspace_size() bytes,
+ *          256-byte aligned; contents on entry are ignored
+ * Uploads the kernel context first if the tree structure changed since the
+ * last call (Section 3.3, lazy copy). B == 0 is a no-op.
+ * Errors: INVALID (table-only cache, null q/o), WORKSPACE, DEVICE. */
+ca_status ca_attention(ca_cache* cache, const void* q, void* o, float scale, void* ws,
+                       size_t ws_bytes, void* stream);
+
+/* Host views of the canonical tables for the current tree (see ca_tables).
+ * Lengths reflect every call made so far. */
+ca_status ca_export_tables(const ca_cache* cache, ca_tables* out);
+
+/* Counters for tests and reports: number of kernel-context uploads so far,
+ * slots in use, and total slots. Any pointer may be NULL. */
+ca_status ca_stats(const ca_cache* cache, int64_t* uploads, int64_t* slots_used,
+                   int64_t* slots_total);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char* ca_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CHUNKATTN_H */

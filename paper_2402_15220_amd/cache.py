@@ -1,0 +1,117 @@
+"""Torch-facing wrapper of the C ABI: torch provides device memory and the
+current stream, every step of the attention path runs in the HIP library."""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from . import binding as B
+
+_DT = {torch.float16: B.CA_FP16, torch.float32: B.CA_FP32}
+
+
+class Cache:
+    """A prefix-tree chunked KV cache on one GPU (or table-only on the host).
+
+    Pools are allocated here with torch (layout [slot][head][c][d]) and lent
+    to the library; q/o rows follow ``seq_order()``.
+    """
+
+    def __init__(self, chunk_size: int, num_heads: int, head_dim: int, num_slots: int,
+                 dtype=torch.float16, device="cuda", table_only: bool = False):
+        self.c, self.H, self.d = chunk_size, num_heads, head_dim
+        self.dtype = dtype
+        self.num_slots = num_slots
+        self.table_only = table_only
+        if table_only:
+            self.k_pool = self.v_pool = None
+            self.h = B.ca_create(chunk_size, num_heads, head_dim, _DT[dtype], num_slots)
+        else:
+            shape = (num_slots, num_heads, chunk_size, head_dim)
+            self.k_pool = torch.empty(shape, dtype=dtype, device=device)
+            self.v_pool = torch.empty(shape, dtype=dtype, device=device)
+            self.h = B.ca_create(chunk_size, num_heads, head_dim, _DT[dtype], num_slots,
+                                 self.k_pool.data_ptr(), self.v_pool.data_ptr())
+        self._ws = None
+
+    # -- helpers -----------------------------------------------------------
+    @staticmethod
+    def stream():
+        return torch.cuda.current_stream().cuda_stream
+
+    def _kv(self, k, v, n):
+        if self.table_only:
+            if k is not None or v is not None:
+                raise ValueError("table-only cache takes no K/V")
+            return None, None, None
+        for t in (k, v):
+            if t.dtype != self.dtype or not t.is_cuda or tuple(t.shape) != (n, self.H, self.d) \
+                    or not t.is_contiguous():
+                raise ValueError(f"K/V must be contiguous {self.dtype} [{n},{self.H},{self.d}] on the GPU")
+        return k.data_ptr(), v.data_ptr(), self.stream()
+
+    # -- tree operations ---------------------------------------------------
+    def match(self, tokens) -> int:
+        return B.ca_match(self.h, tokens)
+
+    def insert(self, seq_id, tokens, k=None, v=None) -> int:
+        tokens = np.asarray(tokens, np.int32)
+        kp, vp, s = self._kv(k, v, tokens.shape[0])
+        return B.ca_insert(self.h, seq_id, tokens, kp, vp, s)
+
+    def extend(self, seq_id, tokens, k=None, v=None) -> int:
+        tokens = np.asarray(tokens, np.int32)
+        kp, vp, s = self._kv(k, v, tokens.shape[0])
+        return B.ca_extend(self.h, seq_id, tokens, kp, vp, s)
+
+    def append(self, seq_ids, tokens, k=None, v=None):
+        tokens = np.asarray(tokens, np.int32)
+        kp, vp, s = self._kv(k, v, tokens.shape[0])
+        B.ca_append_batch(self.h, seq_ids, tokens, kp, vp, s)
+
+    def remove(self, seq_id):
+        B.ca_remove(self.h, seq_id)
+
+    def num_seqs(self) -> int:
+        return B.ca_num_seqs(self.h)
+
+    def seq_order(self) -> np.ndarray:
+        return B.ca_seq_order(self.h)
+
+    def tables(self) -> dict:
+        return B.ca_export_tables(self.h)
+
+    def stats(self) -> dict:
+        return B.ca_stats(self.h)
+
+    # -- attention ---------------------------------------------------------
+    def workspace(self):
+        need = B.ca_workspace_size(self.h)
+        if self._ws is None or self._ws.numel() < need:
+            self._ws = torch.empty(max(need, 256), dtype=torch.uint8, device=self.k_pool.device)
+        return self._ws, need
+
+    def attention(self, q, out=None, scale: float = 0.0):
+        """q: [B, H, d] in seq_order(); returns o of the same shape/dtype."""
+        if self.table_only:
+            raise ValueError("table-only cache has no attention")
+        Bn = self.num_seqs()
+        if q.dtype != self.dtype or tuple(q.shape) != (Bn, self.H, self.d) or not q.is_contiguous():
+            raise ValueError(f"q must be contiguous {self.dtype} [{Bn},{self.H},{self.d}]")
+        if out is None:
+            out = torch.empty_like(q)
+        ws, need = self.workspace()
+        B.ca_attention(self.h, q.data_ptr(), out.data_ptr(), scale, ws.data_ptr(), ws.numel(),
+                       self.stream())
+        return out
+
+    def close(self):
+        if self.h is not None:
+            B.ca_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,441 @@
+// C ABI (include/chunkattn.h): host tree + lazy kernel-context upload +
+// kernel launches on the caller's stream.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <string>
+#include <unordered_set>
+#include <vector>
+
+#include "../../include/chunkattn.h"
+#include "kernels.hpp"
+#include "tables.hpp"
+#include "tree.hpp"
+
+namespace {
+
+thread_local std::string g_err;
+
+ca_status fail(ca_status s, const std::string& msg) {
+  g_err = msg;
+  return s;
+}
+
+ca_status from_err(ca::Err e, const char* what) {
+  switch (e) {
+    case ca::Err::ok:
+      return CA_OK;
+    case ca::Err::invalid:
+      return fail(CA_ERR_INVALID, std::string(what) + ": invalid argument");
+    case ca::Err::nomem:
+      return fail(CA_ERR_NOMEM, std::string(what) + ": chunk pool exhausted");
+    case ca::Err::not_found:
+      return fail(CA_ERR_NOT_FOUND, std::string(what) + ": unknown sequence id");
+    case ca::Err::exists:
+      return fail(CA_ERR_EXISTS, std::string(what) + ": sequence id already live");
+  }
+  return fail(CA_ERR_INVALID, what);
+}
+
+ca_status hip_fail(hipError_t e, const char* what) {
+  return fail(CA_ERR_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+int env_int(const char* name, int dflt) {
+  const char* s = std::getenv(name);
+  return s && *s ? std::atoi(s) : dflt;
+}
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+}  // namespace
+
+struct ca_cache {
+  ca_config cfg{};
+  bool table_only = false;
+  ca::ChunkTree tree;
+  ca::Tables tables;
+  ca::WorkLists work;
+  bool work_valid = false;
+  int32_t seg_chunks = 4;
+  int32_t split_chunks = 0;
+
+  // device state
+  int32_t* d_slot_len = nullptr;
+  char* d_blob = nullptr;
+  size_t d_blob_cap = 0;
+  char* h_stage[2] = {nullptr, nullptr};
+  size_t h_stage_cap[2] = {0, 0};
+  hipEvent_t ev[2] = {nullptr, nullptr};
+  bool ev_used[2] = {false, false};
+  int stage = 0;
+  ca::DevWork dw;
+  bool dw_valid = false;
+  int64_t uploads = 0;
+
+  // host export buffers
+  ca::Tables exported;
+
+  explicit ca_cache(const ca_config& c) : cfg(c), tree(c.chunk_size, c.num_slots) {}
+  ~ca_cache() {
+    if (d_slot_len) (void)hipFree(d_slot_len);
+    if (d_blob) (void)hipFree(d_blob);
+    for (int i = 0; i < 2; ++i) {
+      if (h_stage[i]) (void)hipHostFree(h_stage[i]);
+      if (ev[i]) (void)hipEventDestroy(ev[i]);
+    }
+  }
+
+  size_t esize() const { return cfg.dtype == CA_FP16 ? 2 : 4; }
+
+  void ensure_work() {
+    if (work_valid && !tree.dirty()) return;
+    ca::build_tables(tree, &tables);
+    ca::build_work(tree, tables, seg_chunks, split_chunks, &work);
+    work_valid = true;
+    dw_valid = false;
+    tree.clear_dirty();
+  }
+
+  size_t ws_bytes() const {
+    const size_t np = static_cast<size_t>(work.n_parts);
+    const size_t H = cfg.num_heads, D = cfg.head_dim;
+    return align_up(np * H * D * 4, 256) + align_up(np * H * 2 * 4, 256);
+  }
+
+  // Flatten the work lists into one blob and copy it to the device on
+  // `stream` through a double-buffered pinned staging area.
+  ca_status upload(hipStream_t stream) {
+    const auto& W = work;
+    size_t off = 0;
+    auto place = [&](size_t bytes) {
+      const size_t o = off;
+      off = align_up(off + bytes, 16);
+      return o;
+    };
+    const size_t o_segs = place(W.segs.size() * sizeof(ca::CfSeg));
+    const size_t o_seg_slots = place(W.seg_slots.size() * 4);
+    const size_t o_items = place(W.items.size() * sizeof(ca::SfItem));
+    const size_t o_priv = place(W.priv_slot.size() * 4);
+    const size_t o_pptr = place(W.part_ptr.size() * 4);
+    const size_t o_parts = place(W.parts.size() * 4);
+    const size_t o_mg = place(W.mg_rows.size() * 4);
+    const size_t total = std::max<size_t>(off, 16);
+
+    hipError_t e;
+    if (total > d_blob_cap) {
+      if (d_blob) {
+        // kernels already enqueued may still read the old blob
+        if ((e = hipStreamSynchronize(stream)) != hipSuccess) return hip_fail(e, "upload sync");
+        (void)hipFree(d_blob);
+        d_blob = nullptr;
+        d_blob_cap = 0;
+      }
+      const size_t cap = align_up(std::max<size_t>(total * 2, 4096), 4096);
+      if ((e = hipMalloc(reinterpret_cast<void**>(&d_blob), cap)) != hipSuccess)
+        return hip_fail(e, "upload alloc");
+      d_blob_cap = cap;
+    }
+    const int i = stage;
+    stage ^= 1;
+    if (!ev[i]) {
+      if ((e = hipEventCreateWithFlags(&ev[i], hipEventDisableTiming)) != hipSuccess)
+        return hip_fail(e, "upload event");
+    }
+    if (ev_used[i]) {
+      if ((e = hipEventSynchronize(ev[i])) != hipSuccess) return hip_fail(e, "upload wait");
+    }
+    if (total > h_stage_cap[i]) {
+      if (h_stage[i]) (void)hipHostFree(h_stage[i]);
+      h_stage[i] = nullptr;
+      const size_t cap = align_up(std::max<size_t>(total * 2, 4096), 4096);
+      if ((e = hipHostMalloc(reinterpret_cast<void**>(&h_stage[i]), cap, hipHostMallocDefault)) !=
+          hipSuccess) {
+        h_stage_cap[i] = 0;
+        return hip_fail(e, "upload staging");
+      }
+      h_stage_cap[i] = cap;
+    }
+    char* h = h_stage[i];
+    auto put = [&](size_t o, const void* src, size_t bytes) {
+      if (bytes) std::memcpy(h + o, src, bytes);
+    };
+    put(o_segs, W.segs.data(), W.segs.size() * sizeof(ca::CfSeg));
+    put(o_seg_slots, W.seg_slots.data(), W.seg_slots.size() * 4);
+    put(o_items, W.items.data(), W.items.size() * sizeof(ca::SfItem));
+    put(o_priv, W.priv_slot.data(), W.priv_slot.size() * 4);
+    put(o_pptr, W.part_ptr.data(), W.part_ptr.size() * 4);
+    put(o_parts, W.parts.data(), W.parts.size() * 4);
+    put(o_mg, W.mg_rows.data(), W.mg_rows.size() * 4);
+    if ((e = hipMemcpyAsync(d_blob, h, total, hipMemcpyHostToDevice, stream)) != hipSuccess)
+      return hip_fail(e, "upload copy");
+    if ((e = hipEventRecord(ev[i], stream)) != hipSuccess) return hip_fail(e, "upload record");
+    ev_used[i] = true;
+
+    dw.segs = reinterpret_cast<const ca::CfSeg*>(d_blob + o_segs);
+    dw.seg_slots = reinterpret_cast<const int32_t*>(d_blob + o_seg_slots);
+    dw.n_segs = static_cast<int32_t>(W.segs.size());
+    dw.max_seg_rows = W.max_seg_rows;
+    dw.items = reinterpret_cast<const ca::SfItem*>(d_blob + o_items);
+    dw.n_items = static_cast<int32_t>(W.items.size());
+    dw.priv_slot = reinterpret_cast<const int32_t*>(d_blob + o_priv);
+    dw.part_ptr = reinterpret_cast<const int32_t*>(d_blob + o_pptr);
+    dw.parts = reinterpret_cast<const int32_t*>(d_blob + o_parts);
+    dw.mg_rows = reinterpret_cast<const int32_t*>(d_blob + o_mg);
+    dw.n_mg = static_cast<int32_t>(W.mg_rows.size());
+    dw_valid = true;
+    ++uploads;
+    return CA_OK;
+  }
+
+  // Enqueue K/V copies. Jobs are batched per launch; a job that touches a
+  // slot already touched by the pending batch starts a new launch, so copies
+  // within one launch never depend on each other.
+  ca_status run_jobs(const std::vector<ca::KvJob>& jobs, const void* k, const void* v,
+                     hipStream_t stream) {
+    if (table_only || jobs.empty()) return CA_OK;
+    std::vector<ca::KvJob> batch;
+    std::unordered_set<int32_t> touched;
+    auto flush = [&]() -> ca_status {
+      if (batch.empty()) return CA_OK;
+      hipError_t e = ca::launch_kv_jobs(batch.data(), static_cast<int>(batch.size()),
+                                        cfg.dtype == CA_FP16 ? 0 : 1, cfg.num_heads, cfg.head_dim,
+                                        cfg.chunk_size, k, v, cfg.k_pool, cfg.v_pool, d_slot_len,
+                                        stream);
+      batch.clear();
+      touched.clear();
+      if (e != hipSuccess) return hip_fail(e, "kv copy launch");
+      return CA_OK;
+    };
+    for (const auto& j : jobs) {
+      const bool hazard = touched.count(j.dst_slot) || (j.kind == 1 && touched.count(j.src));
+      if (hazard || static_cast<int>(batch.size()) == ca::kKvJobsPerLaunch) {
+        ca_status s = flush();
+        if (s != CA_OK) return s;
+      }
+      batch.push_back(j);
+      touched.insert(j.dst_slot);
+      if (j.kind == 1) touched.insert(j.src);
+    }
+    return flush();
+  }
+};
+
+extern "C" {
+
+const char* ca_last_error(void) { return g_err.c_str(); }
+
+ca_status ca_create(const ca_config* cfg, ca_cache** out) {
+  if (!cfg || !out) return fail(CA_ERR_INVALID, "ca_create: null argument");
+  if (cfg->chunk_size < 1) return fail(CA_ERR_INVALID, "ca_create: chunk_size < 1");
+  if (cfg->num_heads < 1) return fail(CA_ERR_INVALID, "ca_create: num_heads < 1");
+  if (cfg->head_dim != 64 && cfg->head_dim != 128)
+    return fail(CA_ERR_INVALID, "ca_create: head_dim must be 64 or 128");
+  if (cfg->dtype != CA_FP16 && cfg->dtype != CA_FP32)
+    return fail(CA_ERR_INVALID, "ca_create: bad dtype");
+  if (cfg->num_slots < 1 || cfg->num_slots > INT32_MAX)
+    return fail(CA_ERR_INVALID, "ca_create: num_slots out of range");
+  if ((cfg->k_pool == nullptr) != (cfg->v_pool == nullptr))
+    return fail(CA_ERR_INVALID, "ca_create: give both pools or neither");
+  if ((reinterpret_cast<uintptr_t>(cfg->k_pool) | reinterpret_cast<uintptr_t>(cfg->v_pool)) & 15)
+    return fail(CA_ERR_INVALID, "ca_create: pools must be 16-byte aligned");
+  ca_cache* c = new (std::nothrow) ca_cache(*cfg);
+  if (!c) return fail(CA_ERR_INVALID, "ca_create: out of host memory");
+  c->table_only = cfg->k_pool == nullptr;
+  c->seg_chunks = std::max(1, env_int("CA_CF_SEG", 4));
+  c->split_chunks = env_int("CA_SPLIT", 0);
+  if (!c->table_only) {
+    hipError_t e = hipMalloc(reinterpret_cast<void**>(&c->d_slot_len),
+                             static_cast<size_t>(cfg->num_slots) * sizeof(int32_t));
+    if (e == hipSuccess) e = hipMemset(c->d_slot_len, 0, static_cast<size_t>(cfg->num_slots) * 4);
+    if (e != hipSuccess) {
+      delete c;
+      return hip_fail(e, "ca_create");
+    }
+  }
+  *out = c;
+  return CA_OK;
+}
+
+ca_status ca_destroy(ca_cache* cache) {
+  delete cache;
+  return CA_OK;
+}
+
+static ca_status check_tokens(const int32_t* tokens, int64_t n, const char* what) {
+  if (!tokens || n < 1 || n > INT32_MAX) return fail(CA_ERR_INVALID, std::string(what) + ": bad tokens");
+  for (int64_t i = 0; i < n; ++i)
+    if (tokens[i] < 0) return fail(CA_ERR_INVALID, std::string(what) + ": negative token");
+  return CA_OK;
+}
+
+static ca_status check_kv(const ca_cache* c, const void* k, const void* v, const char* what) {
+  if (c->table_only) {
+    if (k || v) return fail(CA_ERR_INVALID, std::string(what) + ": table-only cache takes no K/V");
+    return CA_OK;
+  }
+  if (!k || !v) return fail(CA_ERR_INVALID, std::string(what) + ": null K/V");
+  if ((reinterpret_cast<uintptr_t>(k) | reinterpret_cast<uintptr_t>(v)) & 15)
+    return fail(CA_ERR_INVALID, std::string(what) + ": K/V must be 16-byte aligned");
+  return CA_OK;
+}
+
+ca_status ca_match(const ca_cache* cache, const int32_t* tokens, int64_t n, int64_t* matched) {
+  if (!cache || !matched) return fail(CA_ERR_INVALID, "ca_match: null argument");
+  ca_status s = check_tokens(tokens, n, "ca_match");
+  if (s != CA_OK) return s;
+  *matched = cache->tree.match(tokens, n);
+  return CA_OK;
+}
+
+ca_status ca_insert(ca_cache* cache, int64_t seq_id, const int32_t* tokens, int64_t n,
+                    const void* k, const void* v, void* stream, int64_t* matched) {
+  if (!cache) return fail(CA_ERR_INVALID, "ca_insert: null cache");
+  ca_status s = check_tokens(tokens, n, "ca_insert");
+  if (s != CA_OK) return s;
+  if ((s = check_kv(cache, k, v, "ca_insert")) != CA_OK) return s;
+  std::vector<ca::KvJob> jobs;
+  int64_t m = 0;
+  ca::Err e = cache->tree.insert(seq_id, tokens, n, &jobs, &m);
+  if (e != ca::Err::ok) return from_err(e, "ca_insert");
+  if (matched) *matched = m;
+  return cache->run_jobs(jobs, k, v, static_cast<hipStream_t>(stream));
+}
+
+ca_status ca_extend(ca_cache* cache, int64_t seq_id, const int32_t* tokens, int64_t n,
+                    const void* k, const void* v, void* stream, int64_t* matched) {
+  if (!cache) return fail(CA_ERR_INVALID, "ca_extend: null cache");
+  ca_status s = check_tokens(tokens, n, "ca_extend");
+  if (s != CA_OK) return s;
+  if ((s = check_kv(cache, k, v, "ca_extend")) != CA_OK) return s;
+  std::vector<ca::KvJob> jobs;
+  int64_t m = 0;
+  ca::Err e = cache->tree.extend(seq_id, tokens, n, 0, &jobs, &m);
+  if (e != ca::Err::ok) return from_err(e, "ca_extend");
+  if (matched) *matched = m;
+  return cache->run_jobs(jobs, k, v, static_cast<hipStream_t>(stream));
+}
+
+ca_status ca_append_batch(ca_cache* cache, int64_t n_seqs, const int64_t* seq_ids,
+                          const int32_t* tokens, const void* k, const void* v, void* stream) {
+  if (!cache) return fail(CA_ERR_INVALID, "ca_append_batch: null cache");
+  if (n_seqs < 0 || n_seqs > INT32_MAX) return fail(CA_ERR_INVALID, "ca_append_batch: bad n_seqs");
+  if (n_seqs == 0) return CA_OK;
+  if (!seq_ids) return fail(CA_ERR_INVALID, "ca_append_batch: null seq_ids");
+  ca_status s = check_tokens(tokens, n_seqs, "ca_append_batch");
+  if (s != CA_OK) return s;
+  if ((s = check_kv(cache, k, v, "ca_append_batch")) != CA_OK) return s;
+  std::vector<ca::KvJob> jobs;
+  ca::Err e = cache->tree.append_batch(n_seqs, seq_ids, tokens, &jobs);
+  if (e != ca::Err::ok) return from_err(e, "ca_append_batch");
+  return cache->run_jobs(jobs, k, v, static_cast<hipStream_t>(stream));
+}
+
+ca_status ca_remove(ca_cache* cache, int64_t seq_id) {
+  if (!cache) return fail(CA_ERR_INVALID, "ca_remove: null cache");
+  return from_err(cache->tree.remove(seq_id), "ca_remove");
+}
+
+ca_status ca_num_seqs(const ca_cache* cache, int64_t* B) {
+  if (!cache || !B) return fail(CA_ERR_INVALID, "ca_num_seqs: null argument");
+  *B = cache->tree.num_seqs();
+  return CA_OK;
+}
+
+ca_status ca_seq_order(const ca_cache* cache, int64_t* seq_ids, int64_t cap) {
+  if (!cache || (!seq_ids && cache->tree.num_seqs() > 0))
+    return fail(CA_ERR_INVALID, "ca_seq_order: null argument");
+  if (cap < cache->tree.num_seqs()) return fail(CA_ERR_INVALID, "ca_seq_order: cap < B");
+  ca_cache* c = const_cast<ca_cache*>(cache);
+  c->ensure_work();
+  std::copy(c->tables.row_seq.begin(), c->tables.row_seq.end(), seq_ids);
+  return CA_OK;
+}
+
+ca_status ca_workspace_size(const ca_cache* cache, size_t* bytes) {
+  if (!cache || !bytes) return fail(CA_ERR_INVALID, "ca_workspace_size: null argument");
+  ca_cache* c = const_cast<ca_cache*>(cache);
+  c->ensure_work();
+  *bytes = c->ws_bytes();
+  return CA_OK;
+}
+
+ca_status ca_attention(ca_cache* cache, const void* q, void* o, float scale, void* ws,
+                       size_t ws_bytes, void* stream) {
+  if (!cache) return fail(CA_ERR_INVALID, "ca_attention: null cache");
+  if (cache->table_only) return fail(CA_ERR_INVALID, "ca_attention: table-only cache");
+  if (cache->tree.num_seqs() == 0) return CA_OK;
+  if (!q || !o) return fail(CA_ERR_INVALID, "ca_attention: null q/o");
+  if ((reinterpret_cast<uintptr_t>(q) | reinterpret_cast<uintptr_t>(o)) & 15)
+    return fail(CA_ERR_INVALID, "ca_attention: q/o must be 16-byte aligned");
+  if (!(scale >= 0.f) || std::isinf(scale)) return fail(CA_ERR_INVALID, "ca_attention: bad scale");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  cache->ensure_work();
+  const size_t need = cache->ws_bytes();
+  if (cache->work.n_parts > 0 && (!ws || ws_bytes < need || (reinterpret_cast<uintptr_t>(ws) & 255)))
+    return fail(CA_ERR_WORKSPACE, "ca_attention: workspace missing, misaligned or smaller than " +
+                                      std::to_string(need) + " bytes");
+  if (!cache->dw_valid) {
+    ca_status st = cache->upload(s);
+    if (st != CA_OK) return st;
+  }
+  const float sc = scale == 0.f ? 1.f / std::sqrt(static_cast<float>(cache->cfg.head_dim)) : scale;
+  ca::AttnArgs a{};
+  a.dtype = cache->cfg.dtype == CA_FP16 ? 0 : 1;
+  a.H = cache->cfg.num_heads;
+  a.D = cache->cfg.head_dim;
+  a.C = cache->cfg.chunk_size;
+  a.q = q;
+  a.o = o;
+  a.kpool = cache->cfg.k_pool;
+  a.vpool = cache->cfg.v_pool;
+  a.slot_len = cache->d_slot_len;
+  const size_t np = static_cast<size_t>(cache->work.n_parts);
+  a.ws_o = static_cast<float*>(ws);
+  a.ws_ml = np ? reinterpret_cast<float*>(static_cast<char*>(ws) +
+                                          align_up(np * a.H * a.D * 4, 256))
+               : nullptr;
+  a.qscale = sc * 1.4426950408889634f;
+  hipError_t e = ca::launch_attention(a, cache->dw, s, env_int("CA_PHASES", 7));
+  if (e != hipSuccess) return hip_fail(e, "ca_attention launch");
+  return CA_OK;
+}
+
+ca_status ca_export_tables(const ca_cache* cache, ca_tables* out) {
+  if (!cache || !out) return fail(CA_ERR_INVALID, "ca_export_tables: null argument");
+  ca_cache* c = const_cast<ca_cache*>(cache);
+  ca::build_tables(c->tree, &c->exported);
+  const ca::Tables& T = c->exported;
+  out->B = static_cast<int64_t>(T.row_seq.size());
+  out->n_nodes = static_cast<int64_t>(T.node_slot.size());
+  out->n_shared = static_cast<int64_t>(T.shr_node.size());
+  out->row_seq = T.row_seq.data();
+  out->node_slot = T.node_slot.data();
+  out->node_len = T.node_len.data();
+  out->node_row_begin = T.node_row_begin.data();
+  out->node_row_end = T.node_row_end.data();
+  out->node_parent = T.node_parent.data();
+  out->node_start_pos = T.node_start_pos.data();
+  out->shr_node = T.shr_node.data();
+  out->shr_part_base = T.shr_part_base.data();
+  out->priv_ptr = T.priv_ptr.data();
+  out->priv_node = T.priv_node.data();
+  out->shr_ptr = T.shr_ptr.data();
+  out->shr_part = T.shr_part.data();
+  return CA_OK;
+}
+
+ca_status ca_stats(const ca_cache* cache, int64_t* uploads, int64_t* slots_used,
+                   int64_t* slots_total) {
+  if (!cache) return fail(CA_ERR_INVALID, "ca_stats: null cache");
+  if (uploads) *uploads = cache->uploads;
+  if (slots_used) *slots_used = cache->tree.pool().in_use();
+  if (slots_total) *slots_total = cache->tree.pool().capacity();
+  return CA_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,52 @@
+// Launch interface of the gfx950 kernels (host side).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "tree.hpp"
+#include "worklist.hpp"
+
+namespace ca {
+
+// Device views of the work lists (pointers into one uploaded blob).
+struct DevWork {
+  const CfSeg* segs = nullptr;
+  const int32_t* seg_slots = nullptr;
+  int32_t n_segs = 0;
+  int32_t max_seg_rows = 0;
+  const SfItem* items = nullptr;
+  int32_t n_items = 0;
+  const int32_t* priv_slot = nullptr;
+  const int32_t* part_ptr = nullptr;
+  const int32_t* parts = nullptr;
+  const int32_t* mg_rows = nullptr;
+  int32_t n_mg = 0;
+};
+
+struct AttnArgs {
+  int dtype;  // 0 fp16, 1 fp32
+  int H, D, C;
+  const void* q;
+  void* o;
+  const void* kpool;
+  const void* vpool;
+  const int32_t* slot_len;
+  float* ws_o;   // [n_parts][H][D]
+  float* ws_ml;  // [n_parts][H][2] (running max in log2 units, sum)
+  float qscale;  // softmax scale * log2(e)
+};
+
+// Enqueue the chunk-first, sequence-first and merge kernels. `phase_mask`
+// selects phases (bit 0 chunk-first, bit 1 sequence-first, bit 2 merge).
+hipError_t launch_attention(const AttnArgs& a, const DevWork& w, hipStream_t stream,
+                            int phase_mask = 7);
+
+// K/V row copies for tree operations (at most kKvJobsPerLaunch per call).
+constexpr int kKvJobsPerLaunch = 64;
+hipError_t launch_kv_jobs(const KvJob* jobs, int n, int dtype, int H, int D, int C,
+                          const void* k, const void* v, void* kpool, void* vpool,
+                          int32_t* slot_len, hipStream_t stream);
+
+}  // namespace ca

@@ -1,0 +1,193 @@
+// Kernel context flattening (ChunkAttention Section 3.3, Figure 2).
+#include "tables.hpp"
+
+#include <algorithm>
+#include <utility>
+
+namespace ca {
+
+void build_tables(const ChunkTree& tree, Tables* out) {
+  Tables& T = *out;
+  const auto& nodes = tree.nodes();
+
+  // Rows and covered ranges: iterative depth-first pre-order. Children are
+  // stored sorted by first token, terminals sorted by id.
+  T.row_seq.clear();
+  std::vector<int32_t> rb(nodes.size(), 0), re(nodes.size(), 0);
+  {
+    std::vector<std::pair<int32_t, bool>> stack;
+    stack.emplace_back(ChunkTree::kRoot, false);
+    while (!stack.empty()) {
+      auto [id, done] = stack.back();
+      stack.pop_back();
+      if (done) {
+        re[id] = static_cast<int32_t>(T.row_seq.size());
+        continue;
+      }
+      rb[id] = static_cast<int32_t>(T.row_seq.size());
+      for (int64_t sid : nodes[id].terminals) T.row_seq.push_back(sid);
+      stack.emplace_back(id, true);
+      const auto& ch = nodes[id].children;
+      for (auto it = ch.rbegin(); it != ch.rend(); ++it) stack.emplace_back(it->second, false);
+    }
+  }
+
+  // Node order: breadth-first levels.
+  T.node_id.clear();
+  for (const auto& ch : nodes[ChunkTree::kRoot].children) T.node_id.push_back(ch.second);
+  for (size_t i = 0; i < T.node_id.size(); ++i)
+    for (const auto& ch : nodes[T.node_id[i]].children) T.node_id.push_back(ch.second);
+  const size_t nn = T.node_id.size();
+  std::vector<int32_t> index(nodes.size(), -1);
+  for (size_t i = 0; i < nn; ++i) index[T.node_id[i]] = static_cast<int32_t>(i);
+
+  T.node_slot.resize(nn);
+  T.node_len.resize(nn);
+  T.node_row_begin.resize(nn);
+  T.node_row_end.resize(nn);
+  T.node_parent.resize(nn);
+  T.node_start_pos.resize(nn);
+  for (size_t i = 0; i < nn; ++i) {
+    const Node& N = nodes[T.node_id[i]];
+    T.node_slot[i] = N.slot;
+    T.node_len[i] = static_cast<int32_t>(N.tokens.size());
+    T.node_row_begin[i] = rb[T.node_id[i]];
+    T.node_row_end[i] = re[T.node_id[i]];
+    if (N.parent == ChunkTree::kRoot) {
+      T.node_parent[i] = -1;
+      T.node_start_pos[i] = 0;
+    } else {
+      const int32_t p = index[N.parent];  // parents precede children in BFS order
+      T.node_parent[i] = p;
+      T.node_start_pos[i] = T.node_start_pos[p] + T.node_len[p];
+    }
+  }
+
+  T.shr_node.clear();
+  T.shr_part_base.clear();
+  std::vector<int32_t> part_base(nn, -1);
+  int32_t acc = 0;
+  for (size_t i = 0; i < nn; ++i) {
+    const int32_t cnt = T.node_row_end[i] - T.node_row_begin[i];
+    if (cnt >= 2) {
+      T.shr_node.push_back(static_cast<int32_t>(i));
+      T.shr_part_base.push_back(acc);
+      part_base[i] = acc;
+      acc += cnt;
+    }
+  }
+
+  const int64_t B = static_cast<int64_t>(T.row_seq.size());
+  T.priv_ptr.assign(1, 0);
+  T.shr_ptr.assign(1, 0);
+  T.priv_node.clear();
+  T.shr_part.clear();
+  T.path_ptr.assign(1, 0);
+  T.path_node.clear();
+  std::vector<int32_t> path;
+  const auto& seqs = tree.seqs();
+  for (int64_t r = 0; r < B; ++r) {
+    path.clear();
+    for (int32_t x = seqs.at(T.row_seq[r]).term; x != ChunkTree::kRoot; x = nodes[x].parent)
+      path.push_back(index[x]);
+    for (auto it = path.rbegin(); it != path.rend(); ++it) {
+      const int32_t i = *it;
+      T.path_node.push_back(i);
+      if (part_base[i] >= 0)
+        T.shr_part.push_back(part_base[i] + static_cast<int32_t>(r) - T.node_row_begin[i]);
+      else
+        T.priv_node.push_back(i);
+    }
+    T.priv_ptr.push_back(static_cast<int32_t>(T.priv_node.size()));
+    T.shr_ptr.push_back(static_cast<int32_t>(T.shr_part.size()));
+    T.path_ptr.push_back(static_cast<int32_t>(T.path_node.size()));
+  }
+}
+
+void build_work(const ChunkTree& tree, const Tables& T, int32_t seg_chunks, int32_t split_chunks,
+                WorkLists* out) {
+  WorkLists& W = *out;
+  const int64_t B = static_cast<int64_t>(T.row_seq.size());
+  const size_t nn = T.node_slot.size();
+  if (seg_chunks < 1) seg_chunks = 1;
+
+  // Runs: a shared node continues its parent's run when the parent is shared
+  // and covers the same rows (BFS order visits parents first).
+  std::vector<int32_t> run_of(nn, -1);
+  std::vector<std::vector<int32_t>> runs;  // node indices root -> leaf
+  for (int32_t i : T.shr_node) {
+    const int32_t p = T.node_parent[i];
+    if (p >= 0 && run_of[p] >= 0 && T.node_row_begin[p] == T.node_row_begin[i] &&
+        T.node_row_end[p] == T.node_row_end[i]) {
+      run_of[i] = run_of[p];
+    } else {
+      run_of[i] = static_cast<int32_t>(runs.size());
+      runs.emplace_back();
+    }
+    runs[run_of[i]].push_back(i);
+  }
+
+  W.segs.clear();
+  W.seg_slots.clear();
+  W.max_seg_rows = 0;
+  std::vector<std::pair<int32_t, int32_t>> run_segs(runs.size());  // [first seg, n segs)
+  int32_t part = 0;
+  for (size_t ru = 0; ru < runs.size(); ++ru) {
+    const auto& chain = runs[ru];
+    const int32_t rb = T.node_row_begin[chain[0]], re = T.node_row_end[chain[0]];
+    run_segs[ru].first = static_cast<int32_t>(W.segs.size());
+    for (size_t s = 0; s < chain.size(); s += seg_chunks) {
+      CfSeg sg{};
+      sg.slot_off = static_cast<int32_t>(W.seg_slots.size());
+      const size_t e = std::min(chain.size(), s + static_cast<size_t>(seg_chunks));
+      for (size_t k = s; k < e; ++k) W.seg_slots.push_back(T.node_slot[chain[k]]);
+      sg.n_chunks = static_cast<int32_t>(e - s);
+      sg.row_begin = rb;
+      sg.row_end = re;
+      sg.part_base = part;
+      part += re - rb;
+      W.max_seg_rows = std::max(W.max_seg_rows, re - rb);
+      W.segs.push_back(sg);
+    }
+    run_segs[ru].second = static_cast<int32_t>(W.segs.size()) - run_segs[ru].first;
+  }
+
+  // Sequence-first items and per-row partial lists.
+  W.items.clear();
+  W.priv_slot.clear();
+  W.part_ptr.assign(1, 0);
+  W.parts.clear();
+  W.mg_rows.clear();
+  (void)tree;
+  for (int64_t r = 0; r < B; ++r) {
+    // segment partials, root -> leaf: each run met along the path once
+    int32_t last_run = -1;
+    for (int32_t k = T.path_ptr[r]; k < T.path_ptr[r + 1]; ++k) {
+      const int32_t ru = run_of[T.path_node[k]];
+      if (ru < 0 || ru == last_run) continue;
+      last_run = ru;
+      for (int32_t s = run_segs[ru].first; s < run_segs[ru].first + run_segs[ru].second; ++s)
+        W.parts.push_back(W.segs[s].part_base + static_cast<int32_t>(r) - W.segs[s].row_begin);
+    }
+    const int32_t pb = static_cast<int32_t>(W.priv_slot.size());
+    for (int32_t k = T.priv_ptr[r]; k < T.priv_ptr[r + 1]; ++k)
+      W.priv_slot.push_back(T.node_slot[T.priv_node[k]]);
+    const int32_t pe = static_cast<int32_t>(W.priv_slot.size());
+    const int32_t np = pe - pb;
+    if (split_chunks <= 0 || np <= split_chunks) {
+      W.items.push_back({static_cast<int32_t>(r), pb, pe, -1});
+    } else {
+      for (int32_t c0 = pb; c0 < pe; c0 += split_chunks) {
+        const int32_t c1 = std::min(pe, c0 + split_chunks);
+        W.items.push_back({static_cast<int32_t>(r), c0, c1, part});
+        W.parts.push_back(part);
+        ++part;
+      }
+      W.mg_rows.push_back(static_cast<int32_t>(r));
+    }
+    W.part_ptr.push_back(static_cast<int32_t>(W.parts.size()));
+  }
+  W.n_parts = part;
+}
+
+}  // namespace ca

@@ -1,0 +1,54 @@
+// Kernel context generated from the tree (ChunkAttention Section 3.3 and
+// Figure 2): canonical tables plus the work lists the kernels consume.
+#pragma once
+
+#include <cstdint>
+#include <vector>
+
+#include "tree.hpp"
+#include "worklist.hpp"
+
+namespace ca {
+
+// Canonical tables (the paper's (C, i, j) context with half-open ranges, plus
+// Algorithm 2's per-sequence lists). Node index = breadth-first level order
+// with children by ascending first token; rows follow a depth-first
+// pre-order in which sequences ending at a node come first (ascending id).
+struct Tables {
+  std::vector<int64_t> row_seq;
+  std::vector<int32_t> node_slot, node_len, node_row_begin, node_row_end, node_parent,
+      node_start_pos;
+  std::vector<int32_t> shr_node, shr_part_base;
+  std::vector<int32_t> priv_ptr, priv_node, shr_ptr, shr_part;
+  std::vector<int32_t> node_id;  // BFS index -> tree node id (internal)
+  std::vector<int32_t> path_ptr, path_node;  // per row, all path nodes root -> leaf (internal)
+};
+
+void build_tables(const ChunkTree& tree, Tables* out);
+
+// Kernel work lists derived from the tables.
+//  * Shared nodes are grouped into runs: maximal parent->child chains of
+//    shared nodes covering the same rows. Each run is cut into segments of at
+//    most seg_chunks chunks; the chunk-first kernel handles one (segment,
+//    head, row block) per workgroup and writes one partial per covered row.
+//  * Each row's private chunks form one sequence-first item, or several of
+//    at most split_chunks chunks (split items write partials that the merge
+//    kernel combines). split_chunks <= 0 disables splitting.
+//  * part lists per row: the row's segment partials root -> leaf, then its
+//    split partials in chunk order.
+struct WorkLists {
+  std::vector<CfSeg> segs;
+  std::vector<int32_t> seg_slots;
+  std::vector<SfItem> items;
+  std::vector<int32_t> priv_slot;  // per row private slots (indexed by items)
+  std::vector<int32_t> part_ptr;   // [B+1]
+  std::vector<int32_t> parts;
+  std::vector<int32_t> mg_rows;    // rows whose result the merge kernel writes
+  int64_t n_parts = 0;
+  int32_t max_seg_rows = 0;
+};
+
+void build_work(const ChunkTree& tree, const Tables& t, int32_t seg_chunks, int32_t split_chunks,
+                WorkLists* out);
+
+}  // namespace ca

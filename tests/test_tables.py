@@ -1,0 +1,223 @@
+"""Host tree of the HIP library against the oracle, bit-exact, on the CPU.
+
+The library runs in table-only mode (no pools, no GPU): every tree operation
+goes through the C ABI and the canonical tables it exports must equal the
+oracle's after every operation. Also: error paths and the exported symbols.
+"""
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import OracleTree, PoolExhausted, tables
+from paper_2402_15220_amd import binding as B
+from workloads import make_dynamic, make_static, random_op_script
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _lib_or_skip():
+    if not os.path.exists(B.LIB_PATH):
+        pytest.fail("library not built: run python -m paper_2402_15220_amd.build")
+    return B.load()
+
+
+def _same(lib_tab, ora_tab):
+    o = ora_tab.as_dict()
+    assert set(lib_tab) == set(o)
+    for k in o:
+        assert np.array_equal(np.asarray(lib_tab[k]), np.asarray(o[k])), k
+
+
+def test_exports_every_declared_symbol():
+    lib = _lib_or_skip()
+    with open(os.path.join(ROOT, "include", "chunkattn.h")) as f:
+        text = f.read()
+    declared = set(re.findall(r"\b(ca_[a-z_]+)\s*\(", text))
+    assert declared == set(B.EXPORTED)
+    for name in declared:
+        assert hasattr(lib, name), name
+
+
+def test_fig2_through_abi():
+    _lib_or_skip()
+    h = B.ca_create(4, 1, 64, B.CA_FP16, 64)
+    t = OracleTree(c=4, with_kv=False)
+    shared = list(range(10, 22))
+    for sid, suf in enumerate([range(30, 34), range(40, 48), range(50, 58)]):
+        toks = np.array(shared + list(suf), np.int32)
+        assert B.ca_insert(h, sid, toks) == t.insert(sid, toks)
+    _same(B.ca_export_tables(h), tables(t))
+    assert list(B.ca_seq_order(h)) == [0, 1, 2]
+    B.ca_destroy(h)
+
+
+def _apply(h, t, op):
+    """Apply one op to both; return the oracle's exception type or None."""
+    err = None
+    try:
+        if op[0] == "insert":
+            r = t.insert(op[1], op[2])
+        elif op[0] == "extend":
+            r = t.extend(op[1], op[2])
+        elif op[0] == "append":
+            r = t.append_batch(op[1], op[2])
+        else:
+            r = t.remove(op[1])
+    except PoolExhausted:
+        err = B.CA_ERR_NOMEM
+        r = None
+    lib_err = None
+    try:
+        if op[0] == "insert":
+            lr = B.ca_insert(h, op[1], op[2])
+        elif op[0] == "extend":
+            lr = B.ca_extend(h, op[1], op[2])
+        elif op[0] == "append":
+            lr = B.ca_append_batch(h, op[1], op[2])
+        else:
+            lr = B.ca_remove(h, op[1])
+    except B.ChunkAttnError as e:
+        lib_err = e.status
+        lr = None
+    assert lib_err == err, (op, lib_err, err)
+    if err is None and op[0] in ("insert", "extend"):
+        assert lr == r
+    return err
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_random_scripts_bit_exact(seed):
+    _lib_or_skip()
+    c = 1 + seed % 5
+    slots = None if seed % 3 else 6 + seed % 7   # some runs with a tight pool
+    n_slots = slots if slots is not None else 1 << 20
+    h = B.ca_create(c, 1, 64, B.CA_FP16, n_slots)
+    t = OracleTree(c=c, num_slots=slots, with_kv=False)
+    live = set()
+    for op in random_op_script(seed, n_ops=80, alphabet=2 + seed % 3, max_len=3 * c + 4):
+        # keep the script valid when a NOMEM insert was refused
+        if op[0] in ("extend", "remove") and op[1] not in live:
+            continue
+        if op[0] == "append":
+            ids = [s for s in op[1] if s in live]
+            if not ids:
+                continue
+            op = ("append", ids, op[2][:len(ids)])
+        err = _apply(h, t, op)
+        if op[0] == "insert" and err is None:
+            live.add(op[1])
+        if op[0] == "remove":
+            live.discard(op[1])
+        t.check_invariants()
+        _same(B.ca_export_tables(h), tables(t))
+        st = B.ca_stats(h)
+        assert st["slots_used"] == t.slots_in_use()
+    B.ca_destroy(h)
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4])
+def test_static_configs_bit_exact(cfg):
+    _lib_or_skip()
+    wl = make_static(cfg)
+    h = B.ca_create(wl.c, wl.H, wl.d, B.CA_FP16, 1 << 16)
+    t = OracleTree(c=wl.c, with_kv=False)
+    for s in wl.seqs:
+        toks = s.tokens(wl.segments)
+        assert B.ca_insert(h, s.seq_id, toks) == t.insert(s.seq_id, toks)
+    _same(B.ca_export_tables(h), tables(t))
+    B.ca_destroy(h)
+
+
+def test_dynamic_config_replay_bit_exact():
+    """Config 5: 64 decode steps with churn; tables equal after every step."""
+    _lib_or_skip()
+    wl = make_dynamic()
+    h = B.ca_create(wl.c, wl.H, wl.d, B.CA_FP16, 1 << 16)
+    t = OracleTree(c=wl.c, with_kv=False)
+    for s in wl.seqs:
+        toks = s.tokens(wl.segments)
+        assert B.ca_insert(h, s.seq_id, toks) == t.insert(s.seq_id, toks)
+    uploads_structural = 0
+    for st in wl.steps():
+        if st.churn:
+            for sid in st.churn.removed:
+                B.ca_remove(h, sid)
+                t.remove(sid)
+            for s in st.churn.added:
+                toks = s.tokens(wl.segments)
+                assert B.ca_insert(h, s.seq_id, toks) == t.insert(s.seq_id, toks) == 2048
+        B.ca_append_batch(h, st.live, st.tokens)
+        t.append_batch(st.live, st.tokens)
+        _same(B.ca_export_tables(h), tables(t))
+        assert list(np.sort(B.ca_seq_order(h))) == list(st.live)
+        uploads_structural += 1
+    t.check_invariants()
+    B.ca_destroy(h)
+
+
+def test_error_paths_leave_state_unchanged():
+    _lib_or_skip()
+    h = B.ca_create(2, 1, 64, B.CA_FP16, 3)
+    B.ca_insert(h, 0, [1, 2, 3, 4])
+    before = B.ca_export_tables(h)
+
+    def unchanged():
+        after = B.ca_export_tables(h)
+        for k in before:
+            assert np.array_equal(before[k], after[k]), k
+
+    cases = [
+        (lambda: B.ca_insert(h, 1, [1, 9, 9, 9]), B.CA_ERR_NOMEM),
+        (lambda: B.ca_insert(h, 0, [5]), B.CA_ERR_EXISTS),
+        (lambda: B.ca_extend(h, 7, [5]), B.CA_ERR_NOT_FOUND),
+        (lambda: B.ca_remove(h, 7), B.CA_ERR_NOT_FOUND),
+        (lambda: B.ca_insert(h, 1, np.zeros(0, np.int32)), B.CA_ERR_INVALID),
+        (lambda: B.ca_insert(h, 1, [3, -1]), B.CA_ERR_INVALID),
+        (lambda: B.ca_extend(h, 0, [5, 6, 7]), B.CA_ERR_NOMEM),
+        (lambda: B.ca_append_batch(h, [0, 0], [1, 1]), B.CA_ERR_INVALID),
+        (lambda: B.ca_append_batch(h, [0, 5], [1, 1]), B.CA_ERR_NOT_FOUND),
+        (lambda: B.ca_attention(h, None, None, 0.0, None, 0), B.CA_ERR_INVALID),
+    ]
+    for fn, status in cases:
+        with pytest.raises(B.ChunkAttnError) as ei:
+            fn()
+        assert ei.value.status == status, ei.value
+        assert B.ca_last_error()
+        unchanged()
+    # NOMEM of a batch that needs two slots with one left: all or nothing
+    B.ca_insert(h, 1, [5])           # takes the last slot; both terminals full
+    before = B.ca_export_tables(h)
+    with pytest.raises(B.ChunkAttnError) as ei:
+        B.ca_append_batch(h, [1, 0], [6, 7])
+    assert ei.value.status == B.CA_ERR_NOMEM
+    unchanged()
+    B.ca_destroy(h)
+
+
+@pytest.mark.parametrize("bad", [
+    dict(chunk_size=0), dict(num_heads=0), dict(head_dim=96), dict(dtype=7), dict(num_slots=0)])
+def test_create_rejects_bad_config(bad):
+    _lib_or_skip()
+    cfg = dict(chunk_size=4, num_heads=1, head_dim=64, dtype=B.CA_FP16, num_slots=8)
+    cfg.update(bad)
+    with pytest.raises(B.ChunkAttnError) as ei:
+        B.ca_create(**cfg)
+    assert ei.value.status == B.CA_ERR_INVALID
+
+
+def test_work_lists_follow_lazy_context_rule():
+    """Section 3.3: the context is rebuilt only on structural change.
+
+    In table-only mode nothing is uploaded, but the workspace size tracks the
+    structure: appends that only fill a private chunk leave it unchanged.
+    """
+    _lib_or_skip()
+    h = B.ca_create(4, 2, 64, B.CA_FP16, 64)
+    B.ca_insert(h, 0, [1, 2, 3, 4, 5])
+    B.ca_insert(h, 1, [1, 2, 3, 4, 6])
+    ws0 = B.ca_workspace_size(h)
+    B.ca_append_batch(h, [0, 1], [7, 7])   # fills the private chunks [5], [6]
+    assert B.ca_workspace_size(h) == ws0
+    B.ca_destroy(h)
