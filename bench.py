@@ -1,0 +1,247 @@
+"""Decode-attention benchmark on one MI355X.
+
+A step is one ca_attention call over the tree of the single-shared-prompt
+workload: B=32 sequences sharing a 1024-token prompt plus 512 unique tokens
+each, H=32, d=128, chunk 64, fp16 (synthetic, seeded; 285.7 MB of K/V, q and
+o per call). The call runs the two-phase partition as one fused launch
+(chunk-first items, then sequence-first items) plus the merge epilogue. The
+tree is built and its kernel context uploaded before timing; inputs are
+resident in HBM.
+
+Prints one JSON line: tokens/s (B per call) and µs per call from the timed
+loop, the roofline of the dominant kernel (the fused two-phase kernel,
+HBM-bound) from HIP events on the launch stream, per-phase figures measured
+in isolation, and the CPU oracle timed on the host for the same workload.
+`--cold` additionally times calls after a clean 1 GiB read that evicts the
+caches (kept out of the default run so profiler averages stay comparable).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+
+def _parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", type=int, default=2, help="workload 2, 3 or 4 (default 2)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle sample time")
+    ap.add_argument("--cold", action="store_true", help="also time calls after a cache-evicting read")
+    ap.add_argument("--seg", type=int, default=0, help="chunk-first segment size (0: library default)")
+    ap.add_argument("--split", type=int, default=-1, help="sequence-first split (-1: library default)")
+    ap.add_argument("--fused", type=int, default=-1, help="1 fused, 0 sequential (-1: default)")
+    return ap.parse_args()
+
+
+def main():
+    args = _parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              "(heads would shard across GPUs with no collective in attention).", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2402_15220_amd.cache import Cache
+    from paper_2402_15220_amd.roofline import PEAK_HBM_GBPS, PEAK_MFMA_TFLOPS, call_model
+    from workloads import make_static
+
+    torch.cuda.set_device(0)
+    wl = make_static(args.config)
+    nodes = sum(-(-len(s) // wl.c) for s in wl.segments)
+    cache = Cache(wl.c, wl.H, wl.d, nodes + 16, dtype=torch.float16)
+    seg_dev = [(torch.from_numpy(s.k).cuda(), torch.from_numpy(s.v).cuda()) for s in wl.segments]
+    for s in wl.seqs:
+        cache.insert(s.seq_id, s.tokens(wl.segments), torch.cat([seg_dev[i][0] for i in s.segs]),
+                     torch.cat([seg_dev[i][1] for i in s.segs]))
+    del seg_dev
+    cache.set_tuning(seg_chunks=args.seg, split_chunks=args.split, fused=args.fused)
+    rows = cache.seq_order()
+    q = torch.from_numpy(np.ascontiguousarray(wl.q[rows])).cuda()
+    o = torch.empty_like(q)
+    model = call_model(cache.tables(), wl.H, wl.d, 2)
+    B = model["B"]
+    torch.cuda.synchronize()
+
+    def call():
+        cache.attention(q, out=o)
+
+    for _ in range(args.warmup):      # also uploads the kernel context
+        call()
+    torch.cuda.synchronize()
+
+    # timed region: exactly `steps` calls, synchronised on both sides
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        call()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms_per_step = elapsed * 1e3 / args.steps
+
+    def back_to_back(fn, n):
+        """Mean device time per fn() over n back-to-back launches, with events
+        on the launch stream (no host synchronisation in between)."""
+        fn()
+        torch.cuda.synchronize()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(n):
+            fn()
+        b.record()
+        b.synchronize()
+        return a.elapsed_time(b) * 1e3 / n
+
+    n_ev = max(args.steps, 50)
+    call_us = back_to_back(call, n_ev)
+    cache.set_tuning(phase_mask=3)        # the fused two-phase kernel alone
+    tpp_us = back_to_back(call, n_ev)
+    cache.set_tuning(phase_mask=4)        # merge epilogue alone (partials already in the workspace)
+    kmg_us = back_to_back(call, n_ev)
+    cache.set_tuning(phase_mask=1)        # chunk-first items alone
+    kcf_us = back_to_back(call, n_ev)
+    cache.set_tuning(phase_mask=2)        # sequence-first items alone
+    ksf_us = back_to_back(call, n_ev)
+    cache.set_tuning(phase_mask=7)
+    call()
+    # a plain device copy of known size (context ceiling, and the reference
+    # kernel for scaling hardware byte counters)
+    src = torch.ones(1 << 28, dtype=torch.float16, device="cuda")   # 512 MiB
+    dst = torch.empty_like(src)
+    copy_us = back_to_back(lambda: dst.copy_(src), 10)
+    copy_bytes = 2 * src.numel() * 2
+    del src, dst
+    torch.cuda.synchronize()
+
+    tpp_bytes = model["shared_kv"] + model["private_kv"] + model["q"]
+    traffic = counter_traffic(wl.name)
+    tpp_gbps = tpp_bytes / (tpp_us * 1e-6) / 1e9
+    ksf_gbps = model["ksf_bytes"] / (ksf_us * 1e-6) / 1e9
+    kcf_tflops = model["kcf_flops"] / (kcf_us * 1e-6) / 1e12
+    us = ms_per_step * 1e3
+    out = {
+        "metric": "decode attention µs/call + tokens/s; achieved HBM GB/s vs peak (B=32,H=32,d=128)",
+        "value": B / (ms_per_step * 1e-3),
+        "unit": "tok/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "B": B, "H": wl.H, "d": wl.d, "c": wl.c,
+                   "shared_tokens": int(model["shared_kv"] // (2 * wl.H * wl.d * 2)),
+                   "private_tokens_per_row": int(model["private_kv"] // (2 * wl.H * wl.d * 2) // B)},
+        "us_per_call": us,
+        "us_per_call_events": call_us,
+        "algorithmic_bytes_per_call": model["total"],
+        "achieved_GBps_per_call": model["total"] / (us * 1e-6) / 1e9,
+        "dense_equivalent_bytes": model["dense_equivalent"],
+        "roofline": {"bound": "hbm", "kernel": "tpp_kernel (fused chunk-first + sequence-first)",
+                     "achieved": tpp_gbps, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                     "frac": tpp_gbps / PEAK_HBM_GBPS, "traffic": traffic,
+                     "bytes_per_launch": tpp_bytes, "us_per_launch": tpp_us},
+        "merge_epilogue_us": kmg_us,
+        "copy_512MiB": {"us": copy_us, "GBps": copy_bytes / (copy_us * 1e-6) / 1e9},
+        "sequence_first_alone": {"kernel": "ksf_kernel", "us_per_launch": ksf_us,
+                                 "bytes_per_launch": model["ksf_bytes"], "GBps": ksf_gbps,
+                                 "frac": ksf_gbps / PEAK_HBM_GBPS},
+        "chunk_first_alone": {"kernel": "kcf_kernel", "us_per_launch": kcf_us,
+                              "flops_per_launch": model["kcf_flops"], "mfma_tflops": kcf_tflops,
+                              "mfma_util": kcf_tflops / PEAK_MFMA_TFLOPS["f16"],
+                              "GBps": (model["shared_kv"] + model["q"]) / (kcf_us * 1e-6) / 1e9},
+    }
+    if args.cold:
+        out["cold"] = cold_times(call, cache, model)
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, rows, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+    cache.close()
+
+
+def counter_traffic(workload):
+    """HBM bytes per tpp_kernel launch from the committed rocprofv3 counter
+    passes (FETCH_SIZE and WRITE_SIZE scaled by a plain copy), or None when
+    the kernels changed since the counters were taken or the workload
+    differs."""
+    import hashlib
+
+    path = os.path.join(ROOT, "profiles", "tpp_kernel_single_prompt_b32_traffic.json")
+    src = os.path.join(ROOT, "paper_2402_15220_amd", "csrc", "kernels.hip")
+    try:
+        with open(path) as f:
+            rec = json.load(f)
+        with open(src, "rb") as f:
+            sha = hashlib.sha256(f.read()).hexdigest()[:16]
+    except OSError:
+        return None
+    if rec.get("kernels_hip_sha256_16") != sha or rec.get("workload") != workload:
+        return None
+    return rec["kernels"]["tpp_kernel"]["traffic_bytes"]
+
+
+def cold_times(call, cache, model, n=30):
+    """Median device time per call after a clean (read-only) 1 GiB pass that
+    evicts L2 and the 256 MB Infinity Cache, events around the call only."""
+    import numpy as np
+    import torch
+
+    flush = torch.ones(1 << 29, dtype=torch.float16, device="cuda")
+    evs = []
+    for _ in range(n):
+        flush.sum()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        call()
+        b.record()
+        evs.append((a, b))
+    torch.cuda.synchronize()
+    us = float(np.median([a.elapsed_time(b) * 1e3 for a, b in evs]))
+    return {"us_per_call": us, "tok_per_s": model["B"] / (us * 1e-6),
+            "GBps": model["total"] / (us * 1e-6) / 1e9}
+
+
+def cpu_baseline(wl, rows, seconds):
+    """The oracle (float64 NumPy) on the same tree and queries, timed on the
+    host. Sample: whole calls (all B rows, all heads), repeated until about
+    `seconds` of CPU time; tree construction is not timed."""
+    import platform
+
+    from oracle import OracleTree, dense_attention_rows
+
+    t = OracleTree(c=wl.c)
+    for s in wl.seqs:
+        k, v = s.kv(wl.segments)
+        t.insert(s.seq_id, s.tokens(wl.segments), k, v)
+    q = wl.q[rows]
+    n = 0
+    t0 = time.perf_counter()
+    while True:
+        dense_attention_rows(t, rows, q, wl.scale)
+        n += 1
+        if time.perf_counter() - t0 >= seconds:
+            break
+    el = time.perf_counter() - t0
+    return {"value": n * len(rows) / el, "unit": "tok/s", "cores": 1, "kind": "oracle",
+            "sample": f"{n} full calls of the workload (B={len(rows)} rows x {wl.H} heads, "
+                      f"float64 NumPy einsum, single-threaded)",
+            "ms_per_call": el * 1e3 / n, "host_cpus": len(os.sched_getaffinity(0)),
+            "cpu": platform.processor() or platform.machine()}
+
+
+if __name__ == "__main__":
+    main()

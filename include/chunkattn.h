@@ -194,6 +194,26 @@ ca_status ca_export_tables(const ca_cache* cache, ca_tables* out);
 ca_status ca_stats(const ca_cache* cache, int64_t* uploads, int64_t* slots_used,
                    int64_t* slots_total);
 
+/* Tuning and per-phase measurement (schedules change speed, not results).
+ *   seg_chunks   shared chunks per chunk-first work item (>= 1; 0 keeps the
+ *                current value). More chunks per item mean fewer partials.
+ *   fused        1: both phases in one launch (chunk-first items first), all
+ *                rows with shared chunks finished by the merge epilogue;
+ *                0: chunk-first launch, then sequence-first launch whose items
+ *                fold the chunk-first partials; -1 keeps the current value.
+ *   split_chunks private chunks per sequence-first work item; rows with more
+ *                private chunks are split and merged by the merge epilogue
+ *                (0 disables splitting, -1 keeps the current value).
+ *   phase_mask   kernels ca_attention enqueues: bit 0 chunk-first, bit 1
+ *                sequence-first, bit 2 merge (0 keeps the current value; the
+ *                default 7 runs all). A subset is for timing one kernel in
+ *                isolation and leaves o incomplete unless the other phases'
+ *                results are already in the workspace.
+ * Changing seg_chunks, split_chunks or fused rebuilds the kernel context and
+ * may change ca_workspace_size. Errors: INVALID. */
+ca_status ca_set_tuning(ca_cache* cache, int32_t seg_chunks, int32_t split_chunks,
+                        int32_t phase_mask, int32_t fused);
+
 /* Message of the last failed call on this thread ("" if none). */
 const char* ca_last_error(void);
 

@@ -30,7 +30,7 @@ CA_FP32 = 1
 
 EXPORTED = ["ca_create", "ca_destroy", "ca_match", "ca_insert", "ca_extend", "ca_append_batch",
             "ca_remove", "ca_num_seqs", "ca_seq_order", "ca_workspace_size", "ca_attention",
-            "ca_export_tables", "ca_stats", "ca_last_error"]
+            "ca_export_tables", "ca_stats", "ca_set_tuning", "ca_last_error"]
 
 
 class ChunkAttnError(RuntimeError):
@@ -86,6 +86,7 @@ def load():
         "ca_attention": [vp, vp, vp, ctypes.c_float, vp, ctypes.c_size_t, vp],
         "ca_export_tables": [vp, ctypes.POINTER(CaTables)],
         "ca_stats": [vp, _P64, _P64, _P64],
+        "ca_set_tuning": [vp, i32, i32, i32, i32],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -213,3 +214,7 @@ def ca_stats(h):
     u, s, t = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
     _check(load().ca_stats(h, ctypes.byref(u), ctypes.byref(s), ctypes.byref(t)))
     return dict(uploads=u.value, slots_used=s.value, slots_total=t.value)
+
+
+def ca_set_tuning(h, seg_chunks=0, split_chunks=-1, phase_mask=0, fused=-1):
+    _check(load().ca_set_tuning(h, seg_chunks, split_chunks, phase_mask, fused))

@@ -84,6 +84,9 @@ class Cache:
     def stats(self) -> dict:
         return B.ca_stats(self.h)
 
+    def set_tuning(self, seg_chunks=0, split_chunks=-1, phase_mask=0, fused=-1):
+        B.ca_set_tuning(self.h, seg_chunks, split_chunks, phase_mask, fused)
+
     # -- attention ---------------------------------------------------------
     def workspace(self):
         need = B.ca_workspace_size(self.h)

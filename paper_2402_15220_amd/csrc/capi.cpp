@@ -63,6 +63,8 @@ struct ca_cache {
   bool work_valid = false;
   int32_t seg_chunks = 4;
   int32_t split_chunks = 0;
+  int32_t phase_mask = 7;
+  bool fused = true;
 
   // device state
   int32_t* d_slot_len = nullptr;
@@ -95,7 +97,7 @@ struct ca_cache {
   void ensure_work() {
     if (work_valid && !tree.dirty()) return;
     ca::build_tables(tree, &tables);
-    ca::build_work(tree, tables, seg_chunks, split_chunks, &work);
+    ca::build_work(tree, tables, seg_chunks, split_chunks, fused, &work);
     work_valid = true;
     dw_valid = false;
     tree.clear_dirty();
@@ -187,6 +189,7 @@ struct ca_cache {
     dw.parts = reinterpret_cast<const int32_t*>(d_blob + o_parts);
     dw.mg_rows = reinterpret_cast<const int32_t*>(d_blob + o_mg);
     dw.n_mg = static_cast<int32_t>(W.mg_rows.size());
+    dw.fused = fused;
     dw_valid = true;
     ++uploads;
     return CA_OK;
@@ -248,6 +251,7 @@ ca_status ca_create(const ca_config* cfg, ca_cache** out) {
   c->table_only = cfg->k_pool == nullptr;
   c->seg_chunks = std::max(1, env_int("CA_CF_SEG", 4));
   c->split_chunks = env_int("CA_SPLIT", 0);
+  c->fused = env_int("CA_FUSED", 1) != 0;
   if (!c->table_only) {
     hipError_t e = hipMalloc(reinterpret_cast<void**>(&c->d_slot_len),
                              static_cast<size_t>(cfg->num_slots) * sizeof(int32_t));
@@ -400,7 +404,7 @@ ca_status ca_attention(ca_cache* cache, const void* q, void* o, float scale, voi
                                           align_up(np * a.H * a.D * 4, 256))
                : nullptr;
   a.qscale = sc * 1.4426950408889634f;
-  hipError_t e = ca::launch_attention(a, cache->dw, s, env_int("CA_PHASES", 7));
+  hipError_t e = ca::launch_attention(a, cache->dw, s, cache->phase_mask);
   if (e != hipSuccess) return hip_fail(e, "ca_attention launch");
   return CA_OK;
 }
@@ -426,6 +430,30 @@ ca_status ca_export_tables(const ca_cache* cache, ca_tables* out) {
   out->priv_node = T.priv_node.data();
   out->shr_ptr = T.shr_ptr.data();
   out->shr_part = T.shr_part.data();
+  return CA_OK;
+}
+
+ca_status ca_set_tuning(ca_cache* cache, int32_t seg_chunks, int32_t split_chunks,
+                        int32_t phase_mask, int32_t fused) {
+  if (!cache) return fail(CA_ERR_INVALID, "ca_set_tuning: null cache");
+  if (seg_chunks < 0 || split_chunks < -1 || phase_mask < 0 || phase_mask > 7 || fused < -1 ||
+      fused > 1)
+    return fail(CA_ERR_INVALID, "ca_set_tuning: value out of range");
+  bool rebuild = false;
+  if (fused >= 0 && (fused == 1) != cache->fused) {
+    cache->fused = fused == 1;
+    rebuild = true;
+  }
+  if (seg_chunks > 0 && seg_chunks != cache->seg_chunks) {
+    cache->seg_chunks = seg_chunks;
+    rebuild = true;
+  }
+  if (split_chunks >= 0 && split_chunks != cache->split_chunks) {
+    cache->split_chunks = split_chunks;
+    rebuild = true;
+  }
+  if (phase_mask > 0) cache->phase_mask = phase_mask;
+  if (rebuild) cache->work_valid = false;
   return CA_OK;
 }
 

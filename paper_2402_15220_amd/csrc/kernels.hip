@@ -7,6 +7,10 @@
 // Softmax runs in base 2: scores are multiplied by scale*log2(e), so partial
 // maxima stored in the workspace are in log2 units.
 //
+// Two schedules: the phases as consecutive launches, or both in ONE launch
+// (tpp_kernel) whose first blocks are chunk-first items and the rest
+// sequence-first items, so the latency-bound chunk-first work overlaps the
+// bandwidth-bound stream.
 //   kcf  chunk-first phase (Algorithm 1, Eqn 1). One workgroup per (segment
 //        of shared chunks, head, block of <= 16*NRT covered rows). For every
 //        64-token block of a chunk it forms S^T = K Q^T on the matrix cores
@@ -14,12 +18,13 @@
 //        online softmax per row, and accumulates O^T = V^T P^T, again on the
 //        matrix cores. It writes one unnormalised partial (O, m, n) per row.
 //   ksf  sequence-first phase (Algorithm 2). One workgroup per (row, head,
-//        split): a bandwidth-bound pass over the row's private chunks with
-//        16-byte loads, sub-wavefront DPP reductions for q.k, and per-lane
-//        online softmax; then the row's chunk-first partials are folded in
-//        with attn_reduce (Eqn 2) and O/n is written.
-//   kmg  merge epilogue for rows whose private chunks were split over
-//        several workgroups (Eqn 2 over every partial of the row, then O/n).
+//        piece of the row's private chunks): a bandwidth-bound pass with
+//        16-byte loads, sub-wavefront DPP reductions for q.k and per-lane
+//        online softmax. An item that owns its row folds the row's
+//        chunk-first partials (sequential schedule) and writes O/n; otherwise
+//        it writes a partial.
+//   kmg  merge epilogue (Algorithm 2's attn_reduce over the partials, Eqn 2,
+//        then O/n) for every row that has partials.
 //   kkv  K/V row copies for tree operations (new chunks, split tails).
 #include <hip/hip_runtime.h>
 
@@ -102,6 +107,65 @@ __device__ __forceinline__ void fold(float& m, float& n, float* acc, float mo, f
   m = mm;
 }
 
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) x = fmaxf(x, __shfl_xor(x, off));
+  return x;
+}
+
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off);
+  return x;
+}
+
+__device__ __forceinline__ float readlane_f(float x, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), l));
+}
+
+// attn_reduce (Eqn 2) of partials parts[k0..k1) into (m, n, acc), a whole
+// wavefront cooperating: the lanes read up to 64 partial maxima at once, the
+// common maximum rescales everything once, then every lane accumulates its
+// d-slice [d0, d0+E) of each partial's O (independent loads, in flight
+// together). Call with all 64 lanes active.
+template <int E>
+__device__ __forceinline__ void fold_parts(int k0, int k1, const int32_t* parts, const float* ws_o,
+                                           const float2* ws_ml, int H, int D, int h, int d0,
+                                           int lane, float& m, float& n, float* acc) {
+  for (int b0 = k0; b0 < k1; b0 += 64) {
+    const int nb = min(64, k1 - b0);
+    int pidx = 0;
+    float pm = kNegBig, pn = 0.f;
+    if (lane < nb) {
+      pidx = parts[b0 + lane];
+      const float2 ml = ws_ml[static_cast<size_t>(pidx) * H + h];
+      pm = ml.x;
+      pn = ml.y;
+    }
+    const float M = fmaxf(m, wave_max(pm));
+    const float wself = fast_exp2(m - M);
+    const float wp = lane < nb ? fast_exp2(pm - M) : 0.f;
+    n = n * wself + wave_sum(wp * pn);
+#pragma unroll
+    for (int j = 0; j < E; ++j) acc[j] *= wself;
+#pragma unroll 4
+    for (int k = 0; k < nb; ++k) {
+      const int pk = __builtin_amdgcn_readlane(pidx, k);
+      const float wk = readlane_f(wp, k);
+      const float* po = ws_o + (static_cast<size_t>(pk) * H + h) * D + d0;
+#pragma unroll
+      for (int j = 0; j < E; j += 4) {
+        const float4 x = *reinterpret_cast<const float4*>(po + j);
+        acc[j] = fmaf(wk, x.x, acc[j]);
+        acc[j + 1] = fmaf(wk, x.y, acc[j + 1]);
+        acc[j + 2] = fmaf(wk, x.z, acc[j + 2]);
+        acc[j + 3] = fmaf(wk, x.w, acc[j + 3]);
+      }
+    }
+    m = M;
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Sequence-first phase.
 
@@ -129,7 +193,12 @@ struct KsfParams {
 // of K and of V of the chunk. Each group of LPT lanes keeps its own running
 // (m, n, acc) over the tokens it saw; the groups are combined at the end.
 template <typename T, int D>
-__global__ __launch_bounds__(256) void ksf_kernel(KsfParams P) {
+constexpr int ksf_lds_bytes() {
+  return 4 * (D * sizeof(T) / 16) * (16 / static_cast<int>(sizeof(T)) + 2) * 4;
+}
+
+template <typename T, int D>
+__device__ __forceinline__ void ksf_block(const KsfParams& P, int item, int h, char* lds) {
   using E = Elem<T>;
   constexpr int EPL = E::kPerVec;
   constexpr int LPT = D / EPL;
@@ -138,8 +207,7 @@ __global__ __launch_bounds__(256) void ksf_kernel(KsfParams P) {
   constexpr int U = 64 / TPS;
   static_assert(U >= 1 && TPS * U == 64, "step must cover 64 tokens");
 
-  const SfItem it = P.items[blockIdx.x];
-  const int h = blockIdx.y;
+  const SfItem it = P.items[item];
   const int H = P.H, C = P.C;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int sub = lane % LPT, tr = lane / LPT;
@@ -156,63 +224,106 @@ __global__ __launch_bounds__(256) void ksf_kernel(KsfParams P) {
 #pragma unroll
   for (int j = 0; j < EPL; ++j) acc[j] = 0.f;
 
-  const T* kpool = static_cast<const T*>(P.kpool);
-  const T* vpool = static_cast<const T*>(P.vpool);
-  for (int ci = it.cb; ci < it.ce; ++ci) {
-    const int slot = P.priv_slot[ci];
-    const int len = P.slot_len[slot];
-    const size_t base = (static_cast<size_t>(slot) * H + h) * static_cast<size_t>(C) * D + sub * EPL;
-    const T* kb = kpool + base;
-    const T* vb = vpool + base;
-    for (int t0 = 0; t0 < len; t0 += 64) {
-      uint4 kr[U], vr[U];
+  const T* kpool = static_cast<const T*>(P.kpool) + static_cast<size_t>(h) * C * D + sub * EPL;
+  const T* vpool = static_cast<const T*>(P.vpool) + static_cast<size_t>(h) * C * D + sub * EPL;
+  const size_t slot_stride = static_cast<size_t>(H) * C * D;
+  const int tok_off = w * TPW + tr;  // this lane's token within a step (u = 0)
+
+  auto load_step = [&](uint4* kr, uint4* vr, int slot, int t0, int len) {
+    const T* kb = kpool + slot * slot_stride;
+    const T* vb = vpool + slot * slot_stride;
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int tok = t0 + u * TPS + w * TPW + tr;
-        if (tok < len) {
-          kr[u] = *reinterpret_cast<const uint4*>(kb + static_cast<size_t>(tok) * D);
-          vr[u] = *reinterpret_cast<const uint4*>(vb + static_cast<size_t>(tok) * D);
-        } else {
-          kr[u] = make_uint4(0, 0, 0, 0);
-          vr[u] = make_uint4(0, 0, 0, 0);
+    for (int u = 0; u < U; ++u) {
+      const int tok = t0 + u * TPS + tok_off;
+      if (tok < len) {
+        kr[u] = *reinterpret_cast<const uint4*>(kb + static_cast<size_t>(tok) * D);
+        vr[u] = *reinterpret_cast<const uint4*>(vb + static_cast<size_t>(tok) * D);
+      } else {
+        kr[u] = make_uint4(0, 0, 0, 0);
+        vr[u] = make_uint4(0, 0, 0, 0);
+      }
+    }
+  };
+  // online softmax over one 64-token step (Eqn 1 for the step, folded by Eqn 2)
+  auto do_step = [&](const uint4* kr, const uint4* vr, int t0, int len) {
+    float s[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      float kf[EPL];
+      E::unpack(kr[u], kf);
+      float dot = 0.f;
+#pragma unroll
+      for (int j = 0; j < EPL; ++j) dot = fmaf(qf[j], kf[j], dot);
+      s[u] = group_sum<LPT>(dot);
+    }
+    float mx = kNegBig;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int tok = t0 + u * TPS + tok_off;
+      s[u] = tok < len ? s[u] * P.qscale : -INFINITY;
+      mx = fmaxf(mx, s[u]);
+    }
+    const float mn = fmaxf(m, mx);
+    const float alpha = fast_exp2(m - mn);
+    n *= alpha;
+#pragma unroll
+    for (int j = 0; j < EPL; ++j) acc[j] *= alpha;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const float p = fast_exp2(s[u] - mn);
+      n += p;
+      float vf[EPL];
+      E::unpack(vr[u], vf);
+#pragma unroll
+      for (int j = 0; j < EPL; ++j) acc[j] = fmaf(p, vf[j], acc[j]);
+    }
+    m = mn;
+  };
+
+  // Chunks are taken 64 at a time: lane i holds the slot and length of chunk
+  // i of the group, broadcast with readlane. The next step's K/V loads are
+  // issued before the current step is computed.
+  for (int g0 = it.cb; g0 < it.ce; g0 += 64) {
+    const int gn = min(64, it.ce - g0);
+    int my_slot = 0, my_len = 0;
+    if (lane < gn) {
+      my_slot = P.priv_slot[g0 + lane];
+      my_len = P.slot_len[my_slot];
+    }
+    int j = 0, t0 = 0;
+    int slot = __builtin_amdgcn_readlane(my_slot, 0);
+    int len = __builtin_amdgcn_readlane(my_len, 0);
+    uint4 kr[U], vr[U];
+    load_step(kr, vr, slot, t0, len);
+    while (true) {
+      int j2 = j, t02 = t0 + 64, slot2 = slot, len2 = len;
+      if (t02 >= len) {
+        j2 = j + 1;
+        t02 = 0;
+        if (j2 < gn) {
+          slot2 = __builtin_amdgcn_readlane(my_slot, j2);
+          len2 = __builtin_amdgcn_readlane(my_len, j2);
         }
       }
-      float s[U];
+      const bool more = j2 < gn;
+      uint4 kn[U], vn[U];
+      if (more) load_step(kn, vn, slot2, t02, len2);
+      do_step(kr, vr, t0, len);
+      if (!more) break;
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        float kf[EPL];
-        E::unpack(kr[u], kf);
-        float dot = 0.f;
-#pragma unroll
-        for (int j = 0; j < EPL; ++j) dot = fmaf(qf[j], kf[j], dot);
-        s[u] = group_sum<LPT>(dot);
+        kr[u] = kn[u];
+        vr[u] = vn[u];
       }
-      float mx = kNegBig;
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int tok = t0 + u * TPS + w * TPW + tr;
-        s[u] = tok < len ? s[u] * P.qscale : -INFINITY;
-        mx = fmaxf(mx, s[u]);
-      }
-      const float mn = fmaxf(m, mx);
-      const float alpha = fast_exp2(m - mn);
-      n *= alpha;
-#pragma unroll
-      for (int j = 0; j < EPL; ++j) acc[j] *= alpha;
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const float p = fast_exp2(s[u] - mn);
-        n += p;
-        float vf[EPL];
-        E::unpack(vr[u], vf);
-#pragma unroll
-        for (int j = 0; j < EPL; ++j) acc[j] = fmaf(p, vf[j], acc[j]);
-      }
-      m = mn;
+      j = j2;
+      t0 = t02;
+      slot = slot2;
+      len = len2;
     }
   }
 
-  // combine the token-row groups of this wavefront
+  // combine the token-row groups of this wavefront (every lane of a d-slice
+  // ends with the same state)
 #pragma unroll
   for (int off = LPT; off < 64; off <<= 1) {
     const float mo = __shfl_xor(m, off);
@@ -222,8 +333,8 @@ __global__ __launch_bounds__(256) void ksf_kernel(KsfParams P) {
     for (int j = 0; j < EPL; ++j) ao[j] = __shfl_xor(acc[j], off);
     fold<EPL>(m, n, acc, mo, no, ao);
   }
-  // combine the four wavefronts
-  __shared__ float st[4][LPT][EPL + 2];
+  // combine the four wavefronts in wavefront 0
+  auto st = reinterpret_cast<float (*)[LPT][EPL + 2]>(lds);
   if (tr == 0) {
     st[w][sub][0] = m;
     st[w][sub][1] = n;
@@ -231,33 +342,22 @@ __global__ __launch_bounds__(256) void ksf_kernel(KsfParams P) {
     for (int j = 0; j < EPL; ++j) st[w][sub][2 + j] = acc[j];
   }
   __syncthreads();
-  if (w != 0 || tr != 0) return;
+  if (w != 0) return;
 #pragma unroll
   for (int ww = 1; ww < 4; ++ww) fold<EPL>(m, n, acc, st[ww][sub][0], st[ww][sub][1], &st[ww][sub][2]);
 
   if (it.out_part < 0) {
-    // fold the chunk-first partials of this row (Algorithm 2), then O/n
-    for (int k = P.part_ptr[it.row]; k < P.part_ptr[it.row + 1]; ++k) {
-      const int p = P.parts[k];
-      const float2 ml = P.ws_ml[static_cast<size_t>(p) * H + h];
-      const float* po = P.ws_o + (static_cast<size_t>(p) * H + h) * D + sub * EPL;
-      float ao[EPL];
-#pragma unroll
-      for (int j = 0; j < EPL; j += 4) {
-        const float4 x = *reinterpret_cast<const float4*>(po + j);
-        ao[j] = x.x;
-        ao[j + 1] = x.y;
-        ao[j + 2] = x.z;
-        ao[j + 3] = x.w;
-      }
-      fold<EPL>(m, n, acc, ml.x, ml.y, ao);
-    }
+    // fold the row's chunk-first partials (Algorithm 2), then O/n
+    fold_parts<EPL>(P.part_ptr[it.row], P.part_ptr[it.row + 1], P.parts, P.ws_o, P.ws_ml, H, D,
+                    h, sub * EPL, lane, m, n, acc);
+    if (tr != 0) return;
     const float inv = 1.f / n;
 #pragma unroll
     for (int j = 0; j < EPL; ++j) acc[j] *= inv;
     *reinterpret_cast<uint4*>(static_cast<T*>(P.o) + (static_cast<size_t>(it.row) * H + h) * D +
                               sub * EPL) = E::pack(acc);
   } else {
+    if (tr != 0) return;
     float* po = P.ws_o + (static_cast<size_t>(it.out_part) * H + h) * D + sub * EPL;
 #pragma unroll
     for (int j = 0; j < EPL; j += 4)
@@ -267,7 +367,7 @@ __global__ __launch_bounds__(256) void ksf_kernel(KsfParams P) {
 }
 
 // ---------------------------------------------------------------------------
-// Merge epilogue for split rows.
+// Merge epilogue: rows whose result is spread over several partials.
 
 struct KmgParams {
   void* o;
@@ -281,26 +381,19 @@ struct KmgParams {
 
 template <typename T, int D>
 __global__ __launch_bounds__(64) void kmg_kernel(KmgParams P) {
-  constexpr int E = D / 64;
   const int row = P.mg_rows[blockIdx.x];
   const int h = blockIdx.y, H = P.H;
   const int lane = threadIdx.x;
-  float m = kNegBig, n = 0.f, acc[E];
-#pragma unroll
-  for (int j = 0; j < E; ++j) acc[j] = 0.f;
-  for (int k = P.part_ptr[row]; k < P.part_ptr[row + 1]; ++k) {
-    const int p = P.parts[k];
-    const float2 ml = P.ws_ml[static_cast<size_t>(p) * H + h];
-    const float* po = P.ws_o + (static_cast<size_t>(p) * H + h) * D;
-    float ao[E];
-#pragma unroll
-    for (int j = 0; j < E; ++j) ao[j] = po[lane + 64 * j];
-    fold<E>(m, n, acc, ml.x, ml.y, ao);
-  }
+  // lanes 0..D/4-1 own four consecutive d each; the rest mirror lane % (D/4)
+  const int d0 = (lane % (D / 4)) * 4;
+  float m = kNegBig, n = 0.f, acc[4] = {0.f, 0.f, 0.f, 0.f};
+  fold_parts<4>(P.part_ptr[row], P.part_ptr[row + 1], P.parts, P.ws_o, P.ws_ml, H, D, h, d0, lane,
+                m, n, acc);
+  if (lane >= D / 4) return;
   const float inv = 1.f / n;
-  T* o = static_cast<T*>(P.o) + (static_cast<size_t>(row) * H + h) * D;
+  T* o = static_cast<T*>(P.o) + (static_cast<size_t>(row) * H + h) * D + d0;
 #pragma unroll
-  for (int j = 0; j < E; ++j) o[lane + 64 * j] = static_cast<T>(acc[j] * inv);
+  for (int j = 0; j < 4; ++j) o[j] = static_cast<T>(acc[j] * inv);
 }
 
 // ---------------------------------------------------------------------------
@@ -333,19 +426,24 @@ struct KcfParams {
 // elements so the transposed A-operand reads of four lane groups fall in
 // disjoint banks).
 template <int D, int NRT>
-__global__ __launch_bounds__(256) void kcf_f16_kernel(KcfParams P) {
+constexpr int kcf_f16_lds_bytes() {
+  return 64 * (D + 2) * 2 + 16 * NRT * (64 + 8) * 2 + 4 * 16 * NRT * 4;
+}
+
+template <int D, int NRT>
+__device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z, int h, char* lds) {
   constexpr int KS = D / 32;  // 16x16x32 steps over d for S^T
   constexpr int DT = D / 64;  // 16-wide d tiles per wavefront for O^T
   constexpr int VS = D + 2;   // V row stride in LDS (halves)
   constexpr int PS = 64 + 8;  // P row stride in LDS (halves), keeps 16-byte row alignment
   constexpr int R = 16 * NRT;
-  __shared__ _Float16 v_lds[64 * VS];
-  __shared__ _Float16 p_lds[R * PS];
-  __shared__ float red[4][R];
+  _Float16* v_lds = reinterpret_cast<_Float16*>(lds);
+  _Float16* p_lds = v_lds + 64 * VS;
+  auto red = reinterpret_cast<float (*)[R]>(p_lds + R * PS);
 
-  const CfSeg sg = P.segs[blockIdx.x];
-  const int h = blockIdx.y, H = P.H, C = P.C;
-  const int rb = sg.row_begin + static_cast<int>(blockIdx.z) * R;
+  const CfSeg sg = P.segs[seg];
+  const int H = P.H, C = P.C;
+  const int rb = sg.row_begin + z * R;
   const int nrows = min(R, sg.row_end - rb);
   if (nrows <= 0) return;
   const int nrt = (nrows + 15) / 16;
@@ -507,18 +605,23 @@ __global__ __launch_bounds__(256) void kcf_f16_kernel(KcfParams P) {
 // fp32 chunk-first: the same schedule on the 16x16x4 fp32 matrix-core op.
 // Operands are single floats (A: row l16, k = g; B: column l16, k = g).
 template <int D, int NRT>
-__global__ __launch_bounds__(256) void kcf_f32_kernel(KcfParams P) {
+constexpr int kcf_f32_lds_bytes() {
+  return 64 * (D + 1) * 4 + 16 * NRT * (64 + 1) * 4 + 4 * 16 * NRT * 4;
+}
+
+template <int D, int NRT>
+__device__ __forceinline__ void kcf_f32_block(const KcfParams& P, int seg, int z, int h, char* lds) {
   constexpr int DT = D / 64;
   constexpr int VS = D + 1;
   constexpr int PS = 64 + 1;
   constexpr int R = 16 * NRT;
-  __shared__ float v_lds[64 * VS];
-  __shared__ float p_lds[R * PS];
-  __shared__ float red[4][R];
+  float* v_lds = reinterpret_cast<float*>(lds);
+  float* p_lds = v_lds + 64 * VS;
+  auto red = reinterpret_cast<float (*)[R]>(p_lds + R * PS);
 
-  const CfSeg sg = P.segs[blockIdx.x];
-  const int h = blockIdx.y, H = P.H, C = P.C;
-  const int rb = sg.row_begin + static_cast<int>(blockIdx.z) * R;
+  const CfSeg sg = P.segs[seg];
+  const int H = P.H, C = P.C;
+  const int rb = sg.row_begin + z * R;
   const int nrows = min(R, sg.row_end - rb);
   if (nrows <= 0) return;
   const int nrt = (nrows + 15) / 16;
@@ -689,37 +792,99 @@ __global__ __launch_bounds__(256) void kkv_kernel(KvJobBatch b, const char* k, c
   if (h == 0 && threadIdx.x == 0) slot_len[j.dst_slot] = j.kind == 2 ? j.dst_pos : j.dst_pos + j.n;
 }
 
-template <typename T, int D>
-void launch_kcf_t(const AttnArgs& a, const DevWork& w, hipStream_t s) {
-  KcfParams P{a.q, a.kpool, a.vpool, a.slot_len, w.segs, w.seg_slots, a.ws_o,
-              reinterpret_cast<float2*>(a.ws_ml), a.H, a.C, a.qscale};
-  const int rows = w.max_seg_rows;
-  const int nrt = rows <= 16 ? 1 : rows <= 32 ? 2 : 4;
-  const int zb = (rows + 16 * nrt - 1) / (16 * nrt);
-  const dim3 grid(w.n_segs, a.H, zb);
-  if constexpr (sizeof(T) == 2) {
-    if (nrt == 1) kcf_f16_kernel<D, 1><<<grid, 256, 0, s>>>(P);
-    else if (nrt == 2) kcf_f16_kernel<D, 2><<<grid, 256, 0, s>>>(P);
-    else kcf_f16_kernel<D, 4><<<grid, 256, 0, s>>>(P);
+// Fused schedule, one launch for both phases: blocks [0, n_cf) run
+// chunk-first work items (dispatched first), the remaining blocks run
+// sequence-first items; both write partial results and the merge epilogue
+// combines them. Sequential schedule: chunk-first launch, then a
+// sequence-first launch whose items fold the finished chunk-first partials
+// themselves (the merge epilogue only finishes split rows).
+struct TppParams {
+  KcfParams cf;
+  KsfParams sf;
+  int n_cf;        // chunk-first blocks: n_segs * zb * H
+  int zb;          // row blocks per segment
+  int block_base;  // first block index of this launch
+};
+
+template <typename T, int D, int NRT>
+constexpr int tpp_lds_bytes() {
+  constexpr int cf = sizeof(T) == 2 ? kcf_f16_lds_bytes<D, NRT>() : kcf_f32_lds_bytes<D, NRT>();
+  constexpr int sf = ksf_lds_bytes<T, D>();
+  return cf > sf ? cf : sf;
+}
+
+template <typename T, int D, int NRT>
+__global__ __launch_bounds__(256, 4) void tpp_kernel(TppParams P) {
+  __shared__ __attribute__((aligned(16))) char lds[tpp_lds_bytes<T, D, NRT>()];
+  const int b = static_cast<int>(blockIdx.x) + P.block_base;
+  const int H = P.sf.H;
+  if (b < P.n_cf) {
+    const int h = b % H;
+    const int rest = b / H;
+    const int z = rest % P.zb;
+    const int seg = rest / P.zb;
+    if constexpr (sizeof(T) == 2)
+      kcf_f16_block<D, NRT>(P.cf, seg, z, h, lds);
+    else
+      kcf_f32_block<D, NRT>(P.cf, seg, z, h, lds);
   } else {
-    if (nrt == 1) kcf_f32_kernel<D, 1><<<grid, 256, 0, s>>>(P);
-    else if (nrt == 2) kcf_f32_kernel<D, 2><<<grid, 256, 0, s>>>(P);
-    else kcf_f32_kernel<D, 4><<<grid, 256, 0, s>>>(P);
+    const int bb = b - P.n_cf;
+    ksf_block<T, D>(P.sf, bb / H, bb % H, lds);
   }
+}
+
+// The phases as separate launches (same block functions, own resources).
+template <typename T, int D, int NRT>
+__global__ __launch_bounds__(256) void kcf_kernel(KcfParams P, int zb) {
+  constexpr int L = sizeof(T) == 2 ? kcf_f16_lds_bytes<D, NRT>() : kcf_f32_lds_bytes<D, NRT>();
+  __shared__ __attribute__((aligned(16))) char lds[L];
+  const int b = static_cast<int>(blockIdx.x);
+  const int h = b % P.H;
+  const int rest = b / P.H;
+  if constexpr (sizeof(T) == 2)
+    kcf_f16_block<D, NRT>(P, rest / zb, rest % zb, h, lds);
+  else
+    kcf_f32_block<D, NRT>(P, rest / zb, rest % zb, h, lds);
+}
+
+template <typename T, int D>
+__global__ __launch_bounds__(256) void ksf_kernel(KsfParams P) {
+  __shared__ __attribute__((aligned(16))) char lds[ksf_lds_bytes<T, D>()];
+  const int b = static_cast<int>(blockIdx.x);
+  ksf_block<T, D>(P, b / P.H, b % P.H, lds);
+}
+
+template <typename T, int D, int NRT>
+void launch_phases(const TppParams& P, int n_sf, bool fused, int mask, hipStream_t s) {
+  if (fused && (mask & 1) && (mask & 2)) {
+    const int grid = P.n_cf + n_sf;
+    if (grid > 0) tpp_kernel<T, D, NRT><<<grid, 256, 0, s>>>(P);
+    return;
+  }
+  if ((mask & 1) && P.n_cf > 0) kcf_kernel<T, D, NRT><<<P.n_cf, 256, 0, s>>>(P.cf, P.zb);
+  if ((mask & 2) && n_sf > 0) ksf_kernel<T, D><<<n_sf, 256, 0, s>>>(P.sf);
 }
 
 template <typename T, int D>
 hipError_t launch_all(const AttnArgs& a, const DevWork& w, hipStream_t s, int mask) {
-  if ((mask & 1) && w.n_segs > 0) launch_kcf_t<T, D>(a, w, s);
-  if ((mask & 2) && w.n_items > 0) {
-    KsfParams P{a.q, a.o, a.kpool, a.vpool, a.slot_len, w.items, w.priv_slot, w.part_ptr, w.parts,
-                a.ws_o, reinterpret_cast<float2*>(a.ws_ml), a.H, a.C, a.qscale};
-    ksf_kernel<T, D><<<dim3(w.n_items, a.H), 256, 0, s>>>(P);
-  }
+  TppParams P;
+  P.cf = KcfParams{a.q, a.kpool, a.vpool, a.slot_len, w.segs, w.seg_slots, a.ws_o,
+                   reinterpret_cast<float2*>(a.ws_ml), a.H, a.C, a.qscale};
+  P.sf = KsfParams{a.q, a.o, a.kpool, a.vpool, a.slot_len, w.items, w.priv_slot, w.part_ptr,
+                   w.parts, a.ws_o, reinterpret_cast<float2*>(a.ws_ml), a.H, a.C, a.qscale};
+  const int rows = w.max_seg_rows;
+  const int nrt = rows <= 16 ? 1 : rows <= 32 ? 2 : 4;
+  P.zb = rows > 0 ? (rows + 16 * nrt - 1) / (16 * nrt) : 1;
+  P.n_cf = w.n_segs * P.zb * a.H;
+  P.block_base = 0;
+  const int n_sf = w.n_items * a.H;
+  if (nrt == 1) launch_phases<T, D, 1>(P, n_sf, w.fused, mask, s);
+  else if (nrt == 2) launch_phases<T, D, 2>(P, n_sf, w.fused, mask, s);
+  else launch_phases<T, D, 4>(P, n_sf, w.fused, mask, s);
   if ((mask & 4) && w.n_mg > 0) {
-    KmgParams P{a.o, w.mg_rows, w.part_ptr, w.parts, a.ws_o, reinterpret_cast<const float2*>(a.ws_ml),
+    KmgParams M{a.o, w.mg_rows, w.part_ptr, w.parts, a.ws_o, reinterpret_cast<const float2*>(a.ws_ml),
                 a.H};
-    kmg_kernel<T, D><<<dim3(w.n_mg, a.H), 64, 0, s>>>(P);
+    kmg_kernel<T, D><<<dim3(w.n_mg, a.H), 64, 0, s>>>(M);
   }
   return hipGetLastError();
 }

@@ -23,6 +23,7 @@ struct DevWork {
   const int32_t* parts = nullptr;
   const int32_t* mg_rows = nullptr;
   int32_t n_mg = 0;
+  bool fused = false;  // one launch for both phases (items then never own a shared row)
 };
 
 struct AttnArgs {

@@ -105,7 +105,7 @@ void build_tables(const ChunkTree& tree, Tables* out) {
 }
 
 void build_work(const ChunkTree& tree, const Tables& T, int32_t seg_chunks, int32_t split_chunks,
-                WorkLists* out) {
+                bool fused, WorkLists* out) {
   WorkLists& W = *out;
   const int64_t B = static_cast<int64_t>(T.row_seq.size());
   const size_t nn = T.node_slot.size();
@@ -174,11 +174,16 @@ void build_work(const ChunkTree& tree, const Tables& T, int32_t seg_chunks, int3
       W.priv_slot.push_back(T.node_slot[T.priv_node[k]]);
     const int32_t pe = static_cast<int32_t>(W.priv_slot.size());
     const int32_t np = pe - pb;
-    if (split_chunks <= 0 || np <= split_chunks) {
+    const bool has_shared = static_cast<int32_t>(W.parts.size()) > W.part_ptr.back();
+    if (!(fused && has_shared) && (split_chunks <= 0 || np <= split_chunks)) {
+      // the row's own item produces its output directly
       W.items.push_back({static_cast<int32_t>(r), pb, pe, -1});
     } else {
-      for (int32_t c0 = pb; c0 < pe; c0 += split_chunks) {
-        const int32_t c1 = std::min(pe, c0 + split_chunks);
+      // chunk-first partials and/or several private pieces: every piece
+      // writes a partial and the merge epilogue produces the output
+      const int32_t piece = split_chunks > 0 ? split_chunks : std::max(np, 1);
+      for (int32_t c0 = pb; c0 < pe; c0 += piece) {
+        const int32_t c1 = std::min(pe, c0 + piece);
         W.items.push_back({static_cast<int32_t>(r), c0, c1, part});
         W.parts.push_back(part);
         ++part;
@@ -187,6 +192,10 @@ void build_work(const ChunkTree& tree, const Tables& T, int32_t seg_chunks, int3
     }
     W.part_ptr.push_back(static_cast<int32_t>(W.parts.size()));
   }
+  // longest items first: they are dispatched first and finish with the rest
+  std::stable_sort(W.items.begin(), W.items.end(), [](const SfItem& a, const SfItem& b) {
+    return a.ce - a.cb > b.ce - b.cb;
+  });
   W.n_parts = part;
 }
 

@@ -32,10 +32,14 @@ void build_tables(const ChunkTree& tree, Tables* out);
 //    most seg_chunks chunks; the chunk-first kernel handles one (segment,
 //    head, row block) per workgroup and writes one partial per covered row.
 //  * Each row's private chunks form one sequence-first item, or several of
-//    at most split_chunks chunks (split items write partials that the merge
-//    kernel combines). split_chunks <= 0 disables splitting.
+//    at most split_chunks chunks (split_chunks <= 0 disables splitting).
+//    An unsplit row is finished by its item (o written directly), which in
+//    the sequential schedule also folds the row's chunk-first partials. In
+//    the fused schedule the chunk-first items run concurrently, so a row with
+//    shared chunks has its item write a partial and the merge epilogue
+//    (mg_rows) finishes it; split rows are always finished by the epilogue.
 //  * part lists per row: the row's segment partials root -> leaf, then its
-//    split partials in chunk order.
+//    sequence-first partials in chunk order.
 struct WorkLists {
   std::vector<CfSeg> segs;
   std::vector<int32_t> seg_slots;
@@ -49,6 +53,6 @@ struct WorkLists {
 };
 
 void build_work(const ChunkTree& tree, const Tables& t, int32_t seg_chunks, int32_t split_chunks,
-                WorkLists* out);
+                bool fused, WorkLists* out);
 
 }  // namespace ca

@@ -1,0 +1,263 @@
+"""GPU parity: the HIP library against the float64 oracle.
+
+Tables and pool contents must match bit-exactly (they are copies); outputs
+must be within max-abs 2e-3 and rel-L2 1e-3 for fp16 inputs (fp32
+accumulation) and within 2e-5 / 1e-5 for fp32 inputs.
+"""
+import numpy as np
+import pytest
+import torch
+
+from parity_util import Pair, assert_close, to_dev
+from paper_2402_15220_amd import binding as B
+from workloads import make_dynamic, make_static, prefix_keyed_kv, random_op_script
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True, scope="module")
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    B.load()
+    yield
+
+
+def _static_pair(wl, slack=16):
+    nodes = sum(-(-len(s) // wl.c) for s in wl.segments)  # aligned configs: one chunk set per segment
+    p = Pair(wl.c, wl.H, wl.d, wl.dtype, nodes + slack)
+    seg_dev = [(to_dev(s.k), to_dev(s.v)) for s in wl.segments]
+    for s in wl.seqs:
+        toks = s.tokens(wl.segments)
+        k, v = s.kv(wl.segments)
+        dk = torch.cat([seg_dev[i][0] for i in s.segs])
+        dv = torch.cat([seg_dev[i][1] for i in s.segs])
+        p.insert(s.seq_id, toks, k, v, dev_k=dk, dev_v=dv)
+    return p
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4])
+def test_static_config(cfg):
+    print(f"[case] static config {cfg}", flush=True)
+    wl = make_static(cfg)
+    p = _static_pair(wl)
+    tb = p.check_tables()
+    p.check_pool(max_nodes=48)
+    o, q, row_seq = p.attention({s.seq_id: wl.q[s.seq_id] for s in wl.seqs})
+    ref = p.reference(row_seq, q, 0.0)
+    assert_close(o, ref, wl.dtype, f"config {cfg} (B={tb['row_seq'].shape[0]})")
+
+
+@pytest.mark.parametrize("seg,split,fused", [(1, 0, 0), (16, 0, 0), (4, 3, 0), (2, 1, 0), (64, 5, 0),
+                                             (1, 0, 1), (4, 0, 1), (16, 3, 1), (3, 1, 1)])
+def test_config2_work_partitions(seg, split, fused):
+    """Every schedule, segment size and split gives the same result."""
+    print(f"[case] config 2 seg={seg} split={split} fused={fused}", flush=True)
+    wl = make_static(2)
+    p = _static_pair(wl)
+    p.cache.set_tuning(seg_chunks=seg, split_chunks=split, fused=fused)
+    o, q, row_seq = p.attention({s.seq_id: wl.q[s.seq_id] for s in wl.seqs})
+    ref = p.reference(row_seq, q, 0.0)
+    assert_close(o, ref, wl.dtype, f"config 2 seg={seg} split={split} fused={fused}")
+
+
+@pytest.mark.timeout(900)
+def test_config5_dynamic_decode():
+    """64 decode steps with churn: tables every step, sampled rows every step."""
+    print("[case] config 5 dynamic", flush=True)
+    wl = make_dynamic()
+    p = Pair(wl.c, wl.H, wl.d, wl.dtype, 2600)
+    seg_dev = {}
+
+    def dev_seg(i):
+        if i not in seg_dev:
+            seg_dev[i] = (to_dev(wl.segments[i].k), to_dev(wl.segments[i].v))
+        return seg_dev[i]
+
+    def insert(s):
+        toks = s.tokens(wl.segments)
+        k, v = s.kv(wl.segments)
+        dk = torch.cat([dev_seg(i)[0] for i in s.segs])
+        dv = torch.cat([dev_seg(i)[1] for i in s.segs])
+        p.insert(s.seq_id, toks, k, v, dev_k=dk, dev_v=dv)
+
+    for s in wl.seqs:
+        insert(s)
+    rng = np.random.default_rng(5)
+    worst = (0.0, 0.0)
+    uploads_before = p.cache.stats()["uploads"]
+    for st in wl.steps():
+        if st.churn:
+            for sid in st.churn.removed:
+                p.remove(sid)
+            for s in st.churn.added:
+                insert(s)
+        p.append(st.live, st.tokens, st.k, st.v)
+        p.check_tables()
+        qmap = {int(sid): st.q[i] for i, sid in enumerate(st.live)}
+        o, q, row_seq = p.attention(qmap)
+        n_rows = len(row_seq) if st.step == 0 else (16 if st.step in (16, 63) else 3)
+        rows = np.sort(rng.choice(len(row_seq), n_rows, replace=False))
+        ref = p.reference(row_seq, q, 0.0, rows=list(rows))
+        ma, rel = assert_close(o[rows], ref, wl.dtype, f"config 5 step {st.step}")
+        worst = (max(worst[0], ma), max(worst[1], rel))
+        if st.step in (0, 17, 63):
+            p.check_pool(max_nodes=32, rng=rng)
+    print(f"[parity] config 5 worst max_abs={worst[0]:.3e} rel_l2={worst[1]:.3e} "
+          f"uploads={p.cache.stats()['uploads'] - uploads_before}", flush=True)
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_random_trees(seed):
+    """Small trees with collisions, splits, partial chunks, removals."""
+    rng = np.random.default_rng(seed)
+    c = [1, 2, 3, 4, 5, 16, 64, 7][seed % 8]
+    d = [64, 128][seed % 2]
+    dtype = [np.float16, np.float32][(seed // 2) % 2]
+    H = 1 + seed % 3
+    print(f"[case] random tree seed={seed} c={c} d={d} H={H} dtype={np.dtype(dtype).name}", flush=True)
+    p = Pair(c, H, d, dtype, 4096)
+    full = {}
+    qrng = np.random.default_rng(1000 + seed)
+    ops = random_op_script(seed, n_ops=50, alphabet=3, max_len=max(12, 2 * c + 3))
+    for i, op in enumerate(ops):
+        if op[0] == "insert":
+            k, v = prefix_keyed_kv(seed, op[2], 0, H, d, dtype)
+            p.insert(op[1], op[2], k, v)
+            full[op[1]] = np.asarray(op[2], np.int32)
+        elif op[0] == "extend":
+            toks = np.concatenate([full[op[1]], op[2]]).astype(np.int32)
+            k, v = prefix_keyed_kv(seed, toks, len(full[op[1]]), H, d, dtype)
+            p.extend(op[1], op[2], k, v)
+            full[op[1]] = toks
+        elif op[0] == "append":
+            ks, vs = [], []
+            for sid, tok in zip(op[1], op[2]):
+                toks = np.concatenate([full[sid], [tok]]).astype(np.int32)
+                k, v = prefix_keyed_kv(seed, toks, len(full[sid]), H, d, dtype)
+                ks.append(k)
+                vs.append(v)
+                full[sid] = toks
+            p.append(op[1], op[2], np.concatenate(ks), np.concatenate(vs))
+        else:
+            p.remove(op[1])
+            del full[op[1]]
+        if full and (i % 5 == 4 or i == len(ops) - 1):
+            p.check_tables()
+            p.check_pool()
+            qmap = {sid: qrng.standard_normal((H, d)).astype(np.float32).astype(dtype) for sid in full}
+            o, q, row_seq = p.attention(qmap)
+            ref = p.reference(row_seq, q, 0.0)
+            assert_close(o, ref, dtype, f"random tree seed={seed} op={i}")
+
+
+def _small_pair(c=4, H=2, d=64, dtype=np.float16):
+    return Pair(c, H, d, dtype, 256)
+
+
+def _kv(rng, n, H, d, dtype):
+    k = rng.standard_normal((n, H, d)).astype(np.float32).astype(dtype)
+    v = rng.standard_normal((n, H, d)).astype(np.float32).astype(dtype)
+    return k, v
+
+
+@pytest.mark.parametrize("dtype", [np.float16, np.float32])
+def test_edge_cases(dtype):
+    print(f"[case] edge cases {np.dtype(dtype).name}", flush=True)
+    rng = np.random.default_rng(11)
+    H, d = 2, 128
+    # B = 1: no shared chunks, plain decode attention
+    p = _small_pair(c=16, H=H, d=d, dtype=dtype)
+    k, v = _kv(rng, 37, H, d, dtype)
+    p.insert(0, np.arange(37), k, v)
+    q = {0: rng.standard_normal((H, d)).astype(dtype)}
+    o, qq, rs = p.attention(q)
+    assert_close(o, p.reference(rs, qq, 0.0), dtype, "B=1")
+    # single-token sequences, all distinct (n_s = 0): o = v
+    p = _small_pair(c=4, H=H, d=d, dtype=dtype)
+    for sid in range(5):
+        k, v = _kv(rng, 1, H, d, dtype)
+        p.insert(sid, [100 + sid], k, v)
+    o, qq, rs = p.attention({sid: rng.standard_normal((H, d)).astype(dtype) for sid in range(5)})
+    for r, sid in enumerate(rs):
+        np.testing.assert_allclose(o[r].astype(np.float64), p.tree.term[int(sid)].v[0].astype(np.float64),
+                                   atol=1e-6)
+    # identical sequences with identical q: identical outputs, every chunk shared
+    p = _small_pair(c=4, H=H, d=d, dtype=dtype)
+    k, v = _kv(rng, 13, H, d, dtype)
+    for sid in range(4):
+        p.insert(sid, np.arange(13), k, v)
+    qv = rng.standard_normal((H, d)).astype(dtype)
+    o, qq, rs = p.attention({sid: qv for sid in range(4)})
+    assert_close(o, p.reference(rs, qq, 0.0), dtype, "identical")
+    assert np.array_equal(o[0], o[1]) and np.array_equal(o[0], o[3])
+    # q = 0 gives the mean of V; a spike key gives that key's V
+    p = _small_pair(c=5, H=H, d=d, dtype=dtype)
+    k, v = _kv(rng, 23, H, d, dtype)
+    qv = rng.standard_normal((H, d)).astype(np.float32)
+    k[9] = (qv * (60.0 * np.sqrt(d) / np.sum(qv ** 2, axis=1, keepdims=True))).astype(dtype)
+    p.insert(0, np.arange(23), k, v)
+    p.insert(1, np.concatenate([np.arange(11), [99, 98]]), *_kv(rng, 13, H, d, dtype))
+    o, qq, rs = p.attention({0: np.zeros((H, d), dtype), 1: qv.astype(dtype)})
+    assert_close(o, p.reference(rs, qq, 0.0), dtype, "q=0 / spike")
+    r0 = int(np.where(rs == 0)[0][0])
+    v0 = np.concatenate([n.v for n in p.tree.path(0)]).astype(np.float64)
+    np.testing.assert_allclose(o[r0].astype(np.float64), v0.mean(axis=0),
+                               atol=2e-3 if dtype == np.float16 else 1e-5)
+    # a sequence that is a prefix of another ends inside a shared chunk
+    p = _small_pair(c=8, H=H, d=d, dtype=dtype)
+    toks = np.arange(20)
+    kk, vv = prefix_keyed_kv(3, toks, 0, H, d, dtype)
+    p.insert(0, toks, kk, vv)
+    p.insert(1, toks[:11], kk[:11], vv[:11])
+    p.insert(2, toks[:3], kk[:3], vv[:3])
+    o, qq, rs = p.attention({sid: rng.standard_normal((H, d)).astype(dtype) for sid in range(3)})
+    assert_close(o, p.reference(rs, qq, 0.0), dtype, "prefix sequences")
+    # non-default scale
+    o, qq, rs = p.attention({sid: rng.standard_normal((H, d)).astype(dtype) for sid in range(3)}, scale=0.37)
+    assert_close(o, p.reference(rs, qq, 0.37), dtype, "scale 0.37")
+
+
+def test_workspace_is_checked():
+    rng = np.random.default_rng(2)
+    p = _small_pair()
+    k, v = _kv(rng, 9, 2, 64, np.float16)
+    p.insert(0, np.arange(9), k, v)
+    p.insert(1, np.arange(9), k, v)
+    need = B.ca_workspace_size(p.cache.h)
+    assert need > 0
+    q = to_dev(rng.standard_normal((2, 2, 64)).astype(np.float16))
+    o = torch.empty_like(q)
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    with pytest.raises(B.ChunkAttnError) as ei:
+        B.ca_attention(p.cache.h, q.data_ptr(), o.data_ptr(), 0.0, ws.data_ptr(), need - 1,
+                       torch.cuda.current_stream().cuda_stream)
+    assert ei.value.status == B.CA_ERR_WORKSPACE
+    B.ca_attention(p.cache.h, q.data_ptr(), o.data_ptr(), 0.0, ws.data_ptr(), need,
+                   torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+
+
+def test_lazy_context_upload():
+    """Section 3.3: the context is re-uploaded only after structural changes."""
+    rng = np.random.default_rng(4)
+    H, d = 2, 64
+    p = _small_pair(c=4, H=H, d=d)
+    k, v = _kv(rng, 6, H, d, np.float16)
+    p.insert(0, np.arange(6), k, v)
+    p.insert(1, np.concatenate([np.arange(4), [50, 51]]), k, v)
+    qmap = lambda: {s: rng.standard_normal((H, d)).astype(np.float16) for s in (0, 1)}  # noqa: E731
+    p.attention(qmap())
+    u0 = p.cache.stats()["uploads"]
+    p.attention(qmap())
+    assert p.cache.stats()["uploads"] == u0          # nothing changed
+    p.append([0, 1], [7, 7], *_kv(rng, 2, H, d, np.float16))   # fills private chunks
+    o, qq, rs = p.attention(qmap())
+    assert p.cache.stats()["uploads"] == u0          # lengths live on the device
+    assert_close(o, p.reference(rs, qq, 0.0), np.float16, "after in-place append")
+    p.append([0, 1], [8, 8], *_kv(rng, 2, H, d, np.float16))   # fills the last free rows
+    o, qq, rs = p.attention(qmap())
+    assert p.cache.stats()["uploads"] == u0
+    p.append([0, 1], [9, 9], *_kv(rng, 2, H, d, np.float16))   # chunks full -> new chunks
+    o, qq, rs = p.attention(qmap())
+    assert p.cache.stats()["uploads"] == u0 + 1
+    assert_close(o, p.reference(rs, qq, 0.0), np.float16, "after chunk growth")
