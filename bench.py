@@ -3,10 +3,10 @@
 A step is one ca_attention call over the tree of the single-shared-prompt
 workload: B=32 sequences sharing a 1024-token prompt plus 512 unique tokens
 each, H=32, d=128, chunk 64, fp16 (synthetic, seeded; 285.7 MB of K/V, q and
-o per call). The call runs the two-phase partition as one fused launch
-(chunk-first items, then sequence-first items) plus the merge epilogue. The
-tree is built and its kernel context uploaded before timing; inputs are
-resident in HBM.
+o per call). By default the call is ONE launch: chunk-first items (dispatched
+first) and sequence-first items in one grid, the last contributor to each
+row merging its partials and writing o. The tree is built and its kernel
+context uploaded before timing; inputs are resident in HBM.
 
 Prints one JSON line: tokens/s (B per call) and µs per call from the timed
 loop, the roofline of the dominant kernel (the fused two-phase kernel,
@@ -38,7 +38,8 @@ def _parse():
     ap.add_argument("--cold", action="store_true", help="also time calls after a cache-evicting read")
     ap.add_argument("--seg", type=int, default=0, help="chunk-first segment size (0: library default)")
     ap.add_argument("--split", type=int, default=-1, help="sequence-first split (-1: library default)")
-    ap.add_argument("--fused", type=int, default=-1, help="1 fused, 0 sequential (-1: default)")
+    ap.add_argument("--schedule", type=int, default=-1,
+                    help="0 sequential, 1 fused launch, 2 concurrent streams (-1: library default)")
     return ap.parse_args()
 
 
@@ -65,12 +66,13 @@ def main():
         cache.insert(s.seq_id, s.tokens(wl.segments), torch.cat([seg_dev[i][0] for i in s.segs]),
                      torch.cat([seg_dev[i][1] for i in s.segs]))
     del seg_dev
-    cache.set_tuning(seg_chunks=args.seg, split_chunks=args.split, fused=args.fused)
+    cache.set_tuning(seg_chunks=args.seg, split_chunks=args.split, schedule=args.schedule)
     rows = cache.seq_order()
     q = torch.from_numpy(np.ascontiguousarray(wl.q[rows])).cuda()
     o = torch.empty_like(q)
     model = call_model(cache.tables(), wl.H, wl.d, 2)
     B = model["B"]
+    stats = cache.stats()
     torch.cuda.synchronize()
 
     def call():
@@ -104,10 +106,8 @@ def main():
 
     n_ev = max(args.steps, 50)
     call_us = back_to_back(call, n_ev)
-    cache.set_tuning(phase_mask=3)        # the fused two-phase kernel alone
+    cache.set_tuning(phase_mask=3)        # the two-phase launch without a separate merge
     tpp_us = back_to_back(call, n_ev)
-    cache.set_tuning(phase_mask=4)        # merge epilogue alone (partials already in the workspace)
-    kmg_us = back_to_back(call, n_ev)
     cache.set_tuning(phase_mask=1)        # chunk-first items alone
     kcf_us = back_to_back(call, n_ev)
     cache.set_tuning(phase_mask=2)        # sequence-first items alone
@@ -150,11 +150,11 @@ def main():
         "algorithmic_bytes_per_call": model["total"],
         "achieved_GBps_per_call": model["total"] / (us * 1e-6) / 1e9,
         "dense_equivalent_bytes": model["dense_equivalent"],
-        "roofline": {"bound": "hbm", "kernel": "tpp_kernel (fused chunk-first + sequence-first)",
+        "schedule": stats["schedule"], "seg_chunks": stats["seg_chunks"],
+        "roofline": {"bound": "hbm", "kernel": "tpp_kernel (fused chunk-first + sequence-first + merge)",
                      "achieved": tpp_gbps, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                      "frac": tpp_gbps / PEAK_HBM_GBPS, "traffic": traffic,
                      "bytes_per_launch": tpp_bytes, "us_per_launch": tpp_us},
-        "merge_epilogue_us": kmg_us,
         "copy_512MiB": {"us": copy_us, "GBps": copy_bytes / (copy_us * 1e-6) / 1e9},
         "sequence_first_alone": {"kernel": "ksf_kernel", "us_per_launch": ksf_us,
                                  "bytes_per_launch": model["ksf_bytes"], "GBps": ksf_gbps,

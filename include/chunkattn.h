@@ -190,17 +190,26 @@ ca_status ca_attention(ca_cache* cache, const void* q, void* o, float scale, voi
 ca_status ca_export_tables(const ca_cache* cache, ca_tables* out);
 
 /* Counters for tests and reports: number of kernel-context uploads so far,
- * slots in use, and total slots. Any pointer may be NULL. */
+ * slots in use, total slots, the attention schedule (see ca_set_tuning) and
+ * the chunk-first segment size of the current kernel context. Any pointer
+ * may be NULL. */
 ca_status ca_stats(const ca_cache* cache, int64_t* uploads, int64_t* slots_used,
-                   int64_t* slots_total);
+                   int64_t* slots_total, int32_t* schedule, int32_t* seg_chunks);
 
 /* Tuning and per-phase measurement (schedules change speed, not results).
- *   seg_chunks   shared chunks per chunk-first work item (>= 1; 0 keeps the
- *                current value). More chunks per item mean fewer partials.
- *   fused        1: both phases in one launch (chunk-first items first), all
- *                rows with shared chunks finished by the merge epilogue;
- *                0: chunk-first launch, then sequence-first launch whose items
- *                fold the chunk-first partials; -1 keeps the current value.
+ *   seg_chunks   shared chunks per chunk-first work item (1..64; 0 keeps the
+ *                current value; -1, the default, sizes segments for about
+ *                one chunk-first block per compute unit, at most 16 chunks).
+ *                More chunks per item mean fewer partials.
+ *   schedule     0: chunk-first launch, then a sequence-first launch whose
+ *                items fold the chunk-first partials; 1: both phases in one
+ *                launch (chunk-first items first), every item writes a
+ *                partial, a merge launch finishes the rows; 2 (default): as
+ *                1 but the last contributor to a row finishes it inside the
+ *                launch; 3: the two phases as concurrent kernels,
+ *                chunk-first on a stream owned by the cache that forks from
+ *                and joins back into the caller's stream, rows finished as
+ *                in 2. -1 keeps the current value.
  *   split_chunks private chunks per sequence-first work item; rows with more
  *                private chunks are split and merged by the merge epilogue
  *                (0 disables splitting, -1 keeps the current value).
@@ -209,10 +218,10 @@ ca_status ca_stats(const ca_cache* cache, int64_t* uploads, int64_t* slots_used,
  *                default 7 runs all). A subset is for timing one kernel in
  *                isolation and leaves o incomplete unless the other phases'
  *                results are already in the workspace.
- * Changing seg_chunks, split_chunks or fused rebuilds the kernel context and
+ * Changing seg_chunks, split_chunks or schedule rebuilds the kernel context and
  * may change ca_workspace_size. Errors: INVALID. */
 ca_status ca_set_tuning(ca_cache* cache, int32_t seg_chunks, int32_t split_chunks,
-                        int32_t phase_mask, int32_t fused);
+                        int32_t phase_mask, int32_t schedule);
 
 /* Message of the last failed call on this thread ("" if none). */
 const char* ca_last_error(void);

@@ -84,8 +84,8 @@ class Cache:
     def stats(self) -> dict:
         return B.ca_stats(self.h)
 
-    def set_tuning(self, seg_chunks=0, split_chunks=-1, phase_mask=0, fused=-1):
-        B.ca_set_tuning(self.h, seg_chunks, split_chunks, phase_mask, fused)
+    def set_tuning(self, seg_chunks=0, split_chunks=-1, phase_mask=0, schedule=-1):
+        B.ca_set_tuning(self.h, seg_chunks, split_chunks, phase_mask, schedule)
 
     # -- attention ---------------------------------------------------------
     def workspace(self):

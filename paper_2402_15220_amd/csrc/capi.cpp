@@ -61,15 +61,19 @@ struct ca_cache {
   ca::Tables tables;
   ca::WorkLists work;
   bool work_valid = false;
-  int32_t seg_chunks = 4;
+  int32_t seg_chunks = 0;  // 0: automatic
+  int32_t num_cus = 256;
   int32_t split_chunks = 0;
   int32_t phase_mask = 7;
-  bool fused = true;
+  int32_t schedule = 2;  // see ca_set_tuning
+  ca::SideStream side;
 
   // device state
   int32_t* d_slot_len = nullptr;
   char* d_blob = nullptr;
   size_t d_blob_cap = 0;
+  int32_t* d_cnt = nullptr;  // [B][H] arrival counters of the partial-writing schedules
+  size_t d_cnt_cap = 0;
   char* h_stage[2] = {nullptr, nullptr};
   size_t h_stage_cap[2] = {0, 0};
   hipEvent_t ev[2] = {nullptr, nullptr};
@@ -86,6 +90,10 @@ struct ca_cache {
   ~ca_cache() {
     if (d_slot_len) (void)hipFree(d_slot_len);
     if (d_blob) (void)hipFree(d_blob);
+    if (d_cnt) (void)hipFree(d_cnt);
+    if (side.fork) (void)hipEventDestroy(side.fork);
+    if (side.join) (void)hipEventDestroy(side.join);
+    if (side.stream) (void)hipStreamDestroy(side.stream);
     for (int i = 0; i < 2; ++i) {
       if (h_stage[i]) (void)hipHostFree(h_stage[i]);
       if (ev[i]) (void)hipEventDestroy(ev[i]);
@@ -97,7 +105,8 @@ struct ca_cache {
   void ensure_work() {
     if (work_valid && !tree.dirty()) return;
     ca::build_tables(tree, &tables);
-    ca::build_work(tree, tables, seg_chunks, split_chunks, fused, &work);
+    ca::build_work(tree, tables, seg_chunks, split_chunks, schedule != 0, cfg.num_heads, num_cus,
+                   &work);
     work_valid = true;
     dw_valid = false;
     tree.clear_dirty();
@@ -189,9 +198,43 @@ struct ca_cache {
     dw.parts = reinterpret_cast<const int32_t*>(d_blob + o_parts);
     dw.mg_rows = reinterpret_cast<const int32_t*>(d_blob + o_mg);
     dw.n_mg = static_cast<int32_t>(W.mg_rows.size());
-    dw.fused = fused;
+    dw.schedule = schedule;
     dw_valid = true;
     ++uploads;
+    return CA_OK;
+  }
+
+  // The concurrent schedule's second stream (default priority) and its
+  // fork/join events, created on first use.
+  ca_status ensure_side() {
+    hipError_t e;
+    if (!side.stream &&
+        (e = hipStreamCreateWithFlags(&side.stream, hipStreamNonBlocking)) != hipSuccess)
+      return hip_fail(e, "side stream");
+    if (!side.fork && (e = hipEventCreateWithFlags(&side.fork, hipEventDisableTiming)) != hipSuccess)
+      return hip_fail(e, "fork event");
+    if (!side.join && (e = hipEventCreateWithFlags(&side.join, hipEventDisableTiming)) != hipSuccess)
+      return hip_fail(e, "join event");
+    return CA_OK;
+  }
+
+  // Arrival counters for B*H (row, head) pairs. They are zeroed once when
+  // allocated; every launch leaves them at zero again.
+  ca_status ensure_counters(size_t n, hipStream_t stream) {
+    if (n <= d_cnt_cap) return CA_OK;
+    hipError_t e;
+    if (d_cnt) {
+      if ((e = hipStreamSynchronize(stream)) != hipSuccess) return hip_fail(e, "counter sync");
+      (void)hipFree(d_cnt);
+      d_cnt = nullptr;
+      d_cnt_cap = 0;
+    }
+    const size_t cap = std::max<size_t>(n * 2, 1024);
+    if ((e = hipMalloc(reinterpret_cast<void**>(&d_cnt), cap * sizeof(int32_t))) != hipSuccess)
+      return hip_fail(e, "counter alloc");
+    if ((e = hipMemsetAsync(d_cnt, 0, cap * sizeof(int32_t), stream)) != hipSuccess)
+      return hip_fail(e, "counter clear");
+    d_cnt_cap = cap;
     return CA_OK;
   }
 
@@ -249,10 +292,15 @@ ca_status ca_create(const ca_config* cfg, ca_cache** out) {
   ca_cache* c = new (std::nothrow) ca_cache(*cfg);
   if (!c) return fail(CA_ERR_INVALID, "ca_create: out of host memory");
   c->table_only = cfg->k_pool == nullptr;
-  c->seg_chunks = std::max(1, env_int("CA_CF_SEG", 4));
+  c->seg_chunks = std::max(0, env_int("CA_CF_SEG", 0));
   c->split_chunks = env_int("CA_SPLIT", 0);
-  c->fused = env_int("CA_FUSED", 1) != 0;
+  c->schedule = std::min(3, std::max(0, env_int("CA_SCHEDULE", 2)));
   if (!c->table_only) {
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+        cus > 0)
+      c->num_cus = cus;
     hipError_t e = hipMalloc(reinterpret_cast<void**>(&c->d_slot_len),
                              static_cast<size_t>(cfg->num_slots) * sizeof(int32_t));
     if (e == hipSuccess) e = hipMemset(c->d_slot_len, 0, static_cast<size_t>(cfg->num_slots) * 4);
@@ -387,6 +435,15 @@ ca_status ca_attention(ca_cache* cache, const void* q, void* o, float scale, voi
     ca_status st = cache->upload(s);
     if (st != CA_OK) return st;
   }
+  if (cache->schedule == 3) {
+    ca_status st = cache->ensure_side();
+    if (st != CA_OK) return st;
+  }
+  {
+    ca_status st = cache->ensure_counters(
+        static_cast<size_t>(cache->tree.num_seqs()) * cache->cfg.num_heads, s);
+    if (st != CA_OK) return st;
+  }
   const float sc = scale == 0.f ? 1.f / std::sqrt(static_cast<float>(cache->cfg.head_dim)) : scale;
   ca::AttnArgs a{};
   a.dtype = cache->cfg.dtype == CA_FP16 ? 0 : 1;
@@ -404,7 +461,8 @@ ca_status ca_attention(ca_cache* cache, const void* q, void* o, float scale, voi
                                           align_up(np * a.H * a.D * 4, 256))
                : nullptr;
   a.qscale = sc * 1.4426950408889634f;
-  hipError_t e = ca::launch_attention(a, cache->dw, s, cache->phase_mask);
+  a.cnt = cache->d_cnt;
+  hipError_t e = ca::launch_attention(a, cache->dw, s, cache->phase_mask, cache->side);
   if (e != hipSuccess) return hip_fail(e, "ca_attention launch");
   return CA_OK;
 }
@@ -434,18 +492,20 @@ ca_status ca_export_tables(const ca_cache* cache, ca_tables* out) {
 }
 
 ca_status ca_set_tuning(ca_cache* cache, int32_t seg_chunks, int32_t split_chunks,
-                        int32_t phase_mask, int32_t fused) {
+                        int32_t phase_mask, int32_t schedule) {
   if (!cache) return fail(CA_ERR_INVALID, "ca_set_tuning: null cache");
-  if (seg_chunks < 0 || split_chunks < -1 || phase_mask < 0 || phase_mask > 7 || fused < -1 ||
-      fused > 1)
+  if (seg_chunks < -1 || seg_chunks > 64 || split_chunks < -1 || phase_mask < 0 || phase_mask > 7 ||
+      schedule < -1 || schedule > 3)
     return fail(CA_ERR_INVALID, "ca_set_tuning: value out of range");
   bool rebuild = false;
-  if (fused >= 0 && (fused == 1) != cache->fused) {
-    cache->fused = fused == 1;
+  if (seg_chunks == -1) seg_chunks = 0;  // automatic
+  else if (seg_chunks == 0) seg_chunks = cache->seg_chunks;
+  if (seg_chunks != cache->seg_chunks) {
+    cache->seg_chunks = seg_chunks;
     rebuild = true;
   }
-  if (seg_chunks > 0 && seg_chunks != cache->seg_chunks) {
-    cache->seg_chunks = seg_chunks;
+  if (schedule >= 0 && schedule != cache->schedule) {
+    cache->schedule = schedule;
     rebuild = true;
   }
   if (split_chunks >= 0 && split_chunks != cache->split_chunks) {
@@ -458,11 +518,17 @@ ca_status ca_set_tuning(ca_cache* cache, int32_t seg_chunks, int32_t split_chunk
 }
 
 ca_status ca_stats(const ca_cache* cache, int64_t* uploads, int64_t* slots_used,
-                   int64_t* slots_total) {
+                   int64_t* slots_total, int32_t* schedule, int32_t* seg_chunks) {
   if (!cache) return fail(CA_ERR_INVALID, "ca_stats: null cache");
   if (uploads) *uploads = cache->uploads;
   if (slots_used) *slots_used = cache->tree.pool().in_use();
   if (slots_total) *slots_total = cache->tree.pool().capacity();
+  if (schedule) *schedule = cache->schedule;
+  if (seg_chunks) {
+    ca_cache* c = const_cast<ca_cache*>(cache);
+    c->ensure_work();
+    *seg_chunks = c->work.seg_chunks;
+  }
   return CA_OK;
 }
 

@@ -123,24 +123,48 @@ __device__ __forceinline__ float readlane_f(float x, int l) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), l));
 }
 
+// Partials are exchanged between blocks of one launch (possibly on different
+// XCDs, each with its own L2) with device-scope stores and loads (`sc1`):
+// they are coherent across XCDs per instruction, so no whole-cache writeback
+// or invalidate is needed. A writer waits for its stores to complete
+// (vmcnt(0)) before counting its arrival.
+__device__ __forceinline__ void st_dev(float* p, float x) {
+  __hip_atomic_store(p, x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_dev4(float* p, float a, float b, float c, float d) {
+  st_dev(p, a);
+  st_dev(p + 1, b);
+  st_dev(p + 2, c);
+  st_dev(p + 3, d);
+}
+__device__ __forceinline__ float ld_dev(const float* p) {
+  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void wait_stores() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
+
 // attn_reduce (Eqn 2) of partials parts[k0..k1) into (m, n, acc), a whole
 // wavefront cooperating: the lanes read up to 64 partial maxima at once, the
 // common maximum rescales everything once, then every lane accumulates its
 // d-slice [d0, d0+E) of each partial's O (independent loads, in flight
 // together). Call with all 64 lanes active.
-template <int E>
+template <int E, bool DEV>
 __device__ __forceinline__ void fold_parts(int k0, int k1, const int32_t* parts, const float* ws_o,
                                            const float2* ws_ml, int H, int D, int h, int d0,
-                                           int lane, float& m, float& n, float* acc) {
+                                           int lane, float& m, float& n, float* acc, int skip = -1) {
   for (int b0 = k0; b0 < k1; b0 += 64) {
     const int nb = min(64, k1 - b0);
     int pidx = 0;
     float pm = kNegBig, pn = 0.f;
-    if (lane < nb) {
+    if (lane < nb && parts[b0 + lane] != skip) {
       pidx = parts[b0 + lane];
-      const float2 ml = ws_ml[static_cast<size_t>(pidx) * H + h];
-      pm = ml.x;
-      pn = ml.y;
+      const float* ml = reinterpret_cast<const float*>(ws_ml + static_cast<size_t>(pidx) * H + h);
+      if constexpr (DEV) {
+        pm = ld_dev(ml);
+        pn = ld_dev(ml + 1);
+      } else {
+        pm = ml[0];
+        pn = ml[1];
+      }
     }
     const float M = fmaxf(m, wave_max(pm));
     const float wself = fast_exp2(m - M);
@@ -150,12 +174,18 @@ __device__ __forceinline__ void fold_parts(int k0, int k1, const int32_t* parts,
     for (int j = 0; j < E; ++j) acc[j] *= wself;
 #pragma unroll 4
     for (int k = 0; k < nb; ++k) {
+      if (parts[b0 + k] == skip) continue;  // uniform
       const int pk = __builtin_amdgcn_readlane(pidx, k);
       const float wk = readlane_f(wp, k);
       const float* po = ws_o + (static_cast<size_t>(pk) * H + h) * D + d0;
 #pragma unroll
       for (int j = 0; j < E; j += 4) {
-        const float4 x = *reinterpret_cast<const float4*>(po + j);
+        float4 x;
+        if constexpr (DEV) {
+          x = make_float4(ld_dev(po + j), ld_dev(po + j + 1), ld_dev(po + j + 2), ld_dev(po + j + 3));
+        } else {
+          x = *reinterpret_cast<const float4*>(po + j);
+        }
         acc[j] = fmaf(wk, x.x, acc[j]);
         acc[j + 1] = fmaf(wk, x.y, acc[j + 1]);
         acc[j + 2] = fmaf(wk, x.z, acc[j + 2]);
@@ -164,6 +194,37 @@ __device__ __forceinline__ void fold_parts(int k0, int k1, const int32_t* parts,
     }
     m = M;
   }
+}
+
+// Finish row `row`, head h from its partials (Eqn 2, then O/n) and write o.
+// One wavefront; lanes [0, D/4) own four consecutive d each. DEV selects
+// device-scope loads (partials written by other blocks of the same launch).
+template <typename T, int D, bool DEV>
+__device__ __forceinline__ void finish_row(const int32_t* part_ptr, const int32_t* parts,
+                                           const float* ws_o, const float2* ws_ml, void* o, int H,
+                                           int row, int h, int lane) {
+  const int d0 = (lane % (D / 4)) * 4;
+  float m = kNegBig, n = 0.f, acc[4] = {0.f, 0.f, 0.f, 0.f};
+  fold_parts<4, DEV>(part_ptr[row], part_ptr[row + 1], parts, ws_o, ws_ml, H, D, h, d0, lane, m, n,
+                     acc);
+  if (lane < D / 4) {
+    const float inv = 1.f / n;
+    T* out = static_cast<T*>(o) + (static_cast<size_t>(row) * H + h) * D + d0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) out[j] = static_cast<T>(acc[j] * inv);
+  }
+}
+
+// Arrival on a (row, head) counter once this block's partials for the row
+// have completed (device-scope stores, then wait_stores()); returns true for
+// the last of the row's `need` contributors, which then finishes the row
+// with device-scope loads. The last arrival resets the counter, so counters
+// are zero between launches.
+__device__ __forceinline__ bool arrive_last(int32_t* c, int need) {
+  const int old = __hip_atomic_fetch_add(c, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (old != need - 1) return false;
+  __hip_atomic_store(c, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return true;
 }
 
 // ---------------------------------------------------------------------------
@@ -184,6 +245,7 @@ struct KsfParams {
   int H;
   int C;
   float qscale;
+  int32_t* cnt;  // partial-writing schedules: per (row, head) arrival counters, else null
 };
 
 // Lane layout: a token row of d elements is read by LPT = d/EPL lanes, 16
@@ -229,19 +291,18 @@ __device__ __forceinline__ void ksf_block(const KsfParams& P, int item, int h, c
   const size_t slot_stride = static_cast<size_t>(H) * C * D;
   const int tok_off = w * TPW + tr;  // this lane's token within a step (u = 0)
 
+  // Loads are unconditional (no branches, so the compiler can count them):
+  // rows past the chunk's length re-read its last row, a finite valid row;
+  // their scores are masked to -inf, so they add exactly 0 * v = 0.
   auto load_step = [&](uint4* kr, uint4* vr, int slot, int t0, int len) {
     const T* kb = kpool + slot * slot_stride;
     const T* vb = vpool + slot * slot_stride;
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int tok = t0 + u * TPS + tok_off;
-      if (tok < len) {
-        kr[u] = *reinterpret_cast<const uint4*>(kb + static_cast<size_t>(tok) * D);
-        vr[u] = *reinterpret_cast<const uint4*>(vb + static_cast<size_t>(tok) * D);
-      } else {
-        kr[u] = make_uint4(0, 0, 0, 0);
-        vr[u] = make_uint4(0, 0, 0, 0);
-      }
+      const size_t row = static_cast<size_t>(min(tok, len - 1)) * D;
+      kr[u] = *reinterpret_cast<const uint4*>(kb + row);
+      vr[u] = *reinterpret_cast<const uint4*>(vb + row);
     }
   };
   // online softmax over one 64-token step (Eqn 1 for the step, folded by Eqn 2)
@@ -281,8 +342,8 @@ __device__ __forceinline__ void ksf_block(const KsfParams& P, int item, int h, c
   };
 
   // Chunks are taken 64 at a time: lane i holds the slot and length of chunk
-  // i of the group, broadcast with readlane. The next step's K/V loads are
-  // issued before the current step is computed.
+  // i of the group, broadcast with readlane (no dependent metadata loads in
+  // the streaming loop).
   for (int g0 = it.cb; g0 < it.ce; g0 += 64) {
     const int gn = min(64, it.ce - g0);
     int my_slot = 0, my_len = 0;
@@ -290,35 +351,14 @@ __device__ __forceinline__ void ksf_block(const KsfParams& P, int item, int h, c
       my_slot = P.priv_slot[g0 + lane];
       my_len = P.slot_len[my_slot];
     }
-    int j = 0, t0 = 0;
-    int slot = __builtin_amdgcn_readlane(my_slot, 0);
-    int len = __builtin_amdgcn_readlane(my_len, 0);
-    uint4 kr[U], vr[U];
-    load_step(kr, vr, slot, t0, len);
-    while (true) {
-      int j2 = j, t02 = t0 + 64, slot2 = slot, len2 = len;
-      if (t02 >= len) {
-        j2 = j + 1;
-        t02 = 0;
-        if (j2 < gn) {
-          slot2 = __builtin_amdgcn_readlane(my_slot, j2);
-          len2 = __builtin_amdgcn_readlane(my_len, j2);
-        }
+    for (int jj = 0; jj < gn; ++jj) {
+      const int slot = __builtin_amdgcn_readlane(my_slot, jj);
+      const int len = __builtin_amdgcn_readlane(my_len, jj);
+      for (int t0 = 0; t0 < len; t0 += 64) {
+        uint4 kr[U], vr[U];
+        load_step(kr, vr, slot, t0, len);
+        do_step(kr, vr, t0, len);
       }
-      const bool more = j2 < gn;
-      uint4 kn[U], vn[U];
-      if (more) load_step(kn, vn, slot2, t02, len2);
-      do_step(kr, vr, t0, len);
-      if (!more) break;
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        kr[u] = kn[u];
-        vr[u] = vn[u];
-      }
-      j = j2;
-      t0 = t02;
-      slot = slot2;
-      len = len2;
     }
   }
 
@@ -348,8 +388,8 @@ __device__ __forceinline__ void ksf_block(const KsfParams& P, int item, int h, c
 
   if (it.out_part < 0) {
     // fold the row's chunk-first partials (Algorithm 2), then O/n
-    fold_parts<EPL>(P.part_ptr[it.row], P.part_ptr[it.row + 1], P.parts, P.ws_o, P.ws_ml, H, D,
-                    h, sub * EPL, lane, m, n, acc);
+    fold_parts<EPL, false>(P.part_ptr[it.row], P.part_ptr[it.row + 1], P.parts, P.ws_o, P.ws_ml, H,
+                           D, h, sub * EPL, lane, m, n, acc);
     if (tr != 0) return;
     const float inv = 1.f / n;
 #pragma unroll
@@ -357,12 +397,51 @@ __device__ __forceinline__ void ksf_block(const KsfParams& P, int item, int h, c
     *reinterpret_cast<uint4*>(static_cast<T*>(P.o) + (static_cast<size_t>(it.row) * H + h) * D +
                               sub * EPL) = E::pack(acc);
   } else {
-    if (tr != 0) return;
-    float* po = P.ws_o + (static_cast<size_t>(it.out_part) * H + h) * D + sub * EPL;
+    if (P.cnt) {
+      // If every other contributor of the row has already arrived (the usual
+      // case: chunk-first items are dispatched first), fold their partials
+      // straight into this item's state and finish the row: no partial, no
+      // arrival. The counter goes back to zero.
+      const int k0 = P.part_ptr[it.row], k1 = P.part_ptr[it.row + 1];
+      int32_t* c = P.cnt + static_cast<size_t>(it.row) * H + h;
+      int ready = 0;
+      if (lane == 0)
+        ready = __hip_atomic_load(c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == k1 - k0 - 1;
+      if (__shfl(ready, 0)) {
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        fold_parts<EPL, true>(k0, k1, P.parts, P.ws_o, P.ws_ml, H, D, h, sub * EPL, lane, m, n, acc,
+                              it.out_part);
+        if (lane == 0) __hip_atomic_store(c, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (tr != 0) return;
+        const float inv = 1.f / n;
 #pragma unroll
-    for (int j = 0; j < EPL; j += 4)
-      *reinterpret_cast<float4*>(po + j) = make_float4(acc[j], acc[j + 1], acc[j + 2], acc[j + 3]);
-    if (sub == 0) P.ws_ml[static_cast<size_t>(it.out_part) * H + h] = make_float2(m, n);
+        for (int j = 0; j < EPL; ++j) acc[j] *= inv;
+        *reinterpret_cast<uint4*>(static_cast<T*>(P.o) + (static_cast<size_t>(it.row) * H + h) * D +
+                                  sub * EPL) = E::pack(acc);
+        return;
+      }
+    }
+    if (tr == 0) {
+      float* po = P.ws_o + (static_cast<size_t>(it.out_part) * H + h) * D + sub * EPL;
+#pragma unroll
+      for (int j = 0; j < EPL; j += 4) st_dev4(po + j, acc[j], acc[j + 1], acc[j + 2], acc[j + 3]);
+      if (sub == 0) {
+        float* pml = reinterpret_cast<float*>(P.ws_ml + static_cast<size_t>(it.out_part) * H + h);
+        st_dev(pml, m);
+        st_dev(pml + 1, n);
+      }
+    }
+    if (P.cnt) {
+      // partial-writing schedules: the last contributor of the row finishes it
+      wait_stores();
+      int last = 0;
+      if (lane == 0) {
+        const int need = P.part_ptr[it.row + 1] - P.part_ptr[it.row];
+        last = arrive_last(P.cnt + static_cast<size_t>(it.row) * H + h, need);
+      }
+      if (__shfl(last, 0))
+        finish_row<T, D, true>(P.part_ptr, P.parts, P.ws_o, P.ws_ml, P.o, H, it.row, h, lane);
+    }
   }
 }
 
@@ -381,19 +460,8 @@ struct KmgParams {
 
 template <typename T, int D>
 __global__ __launch_bounds__(64) void kmg_kernel(KmgParams P) {
-  const int row = P.mg_rows[blockIdx.x];
-  const int h = blockIdx.y, H = P.H;
-  const int lane = threadIdx.x;
-  // lanes 0..D/4-1 own four consecutive d each; the rest mirror lane % (D/4)
-  const int d0 = (lane % (D / 4)) * 4;
-  float m = kNegBig, n = 0.f, acc[4] = {0.f, 0.f, 0.f, 0.f};
-  fold_parts<4>(P.part_ptr[row], P.part_ptr[row + 1], P.parts, P.ws_o, P.ws_ml, H, D, h, d0, lane,
-                m, n, acc);
-  if (lane >= D / 4) return;
-  const float inv = 1.f / n;
-  T* o = static_cast<T*>(P.o) + (static_cast<size_t>(row) * H + h) * D + d0;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) o[j] = static_cast<T>(acc[j] * inv);
+  finish_row<T, D, false>(P.part_ptr, P.parts, P.ws_o, P.ws_ml, P.o, P.H, P.mg_rows[blockIdx.x],
+                          blockIdx.y, threadIdx.x);
 }
 
 // ---------------------------------------------------------------------------
@@ -411,7 +479,41 @@ struct KcfParams {
   int H;
   int C;
   float qscale;
+  // partial-writing schedules only (null otherwise): per (row, head) arrival counters
+  // and what the last contributor needs to finish the row
+  int32_t* cnt;
+  void* o;
+  const int32_t* part_ptr;
+  const int32_t* parts;
 };
+
+// Partial-writing schedules: after a chunk-first block wrote its partials for rows
+// [rb, rb+nrows), count its arrival on each row; rows for which it is the
+// last contributor are finished here, one wavefront per row.
+template <typename T, int D, int R>
+__device__ __forceinline__ void cf_arrive(const KcfParams& P, int rb, int nrows, int h,
+                                          float (*red)[R]) {
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  wait_stores();
+  __syncthreads();  // every wavefront's partial stores have completed
+  unsigned* flags = reinterpret_cast<unsigned*>(&red[0][0]);
+  if (tid < R) {
+    int last = 0;
+    if (tid < nrows) {
+      const int row = rb + tid;
+      last = arrive_last(P.cnt + static_cast<size_t>(row) * P.H + h,
+                         P.part_ptr[row + 1] - P.part_ptr[row]);
+    }
+    flags[tid] = last;
+  }
+  __syncthreads();
+  bool any = false;
+  for (int r = w; r < nrows; r += 4) any |= flags[r] != 0;
+  if (!any) return;
+  for (int r = w; r < nrows; r += 4)
+    if (flags[r])
+      finish_row<T, D, true>(P.part_ptr, P.parts, P.ws_o, P.ws_ml, P.o, P.H, rb + r, h, lane);
+}
 
 // Matrix-core operand layout used below (16x16 output tiles, 64 lanes;
 // l16 = lane % 16, g = lane / 16):
@@ -427,19 +529,43 @@ struct KcfParams {
 // disjoint banks).
 template <int D, int NRT>
 constexpr int kcf_f16_lds_bytes() {
-  return 64 * (D + 2) * 2 + 16 * NRT * (64 + 8) * 2 + 4 * 16 * NRT * 4;
+  constexpr int R = 16 * NRT;
+  constexpr int vb = 4 * 16 * (D + 4) * 2;  // four wavefront V slices
+  constexpr int ob = R * (D + 4) * 4;       // merge buffer (reuses the slices)
+  return (vb > ob ? vb : ob) + 2 * 4 * R * 4;
 }
 
-template <int D, int NRT>
+// Chunk-first block, fp16. Wavefronts work independently: wavefront w owns
+// tokens 16w..16w+15 of every 64-token block of the segment's chunks.
+//   S^T = K Q^T: 16x16x32 MFMA, K rows of its 16 tokens as A, the covered q
+//     rows as B; the lane then holds S^T[token 4g+i][row l16].
+//   online softmax per (wavefront, row): max over its 16 tokens (4 values
+//     per lane, then across the four lane groups by shuffles).
+//   O^T += V^T P^T: 16x16x16 MFMA whose B operand (lane holds k = 4g..4g+3
+//     of column l16) is exactly the layout S^T came out in, so P never leaves
+//     the registers; V^T comes from the wavefront's own 16-token V slice in
+//     LDS (row stride d+4 halves: the four lane groups read disjoint banks).
+// No barrier inside the chunk loop; the four wavefront states are merged
+// once at the end of the segment.
+template <int D, int NRT, typename OUT_T = _Float16>
 __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z, int h, char* lds) {
-  constexpr int KS = D / 32;  // 16x16x32 steps over d for S^T
-  constexpr int DT = D / 64;  // 16-wide d tiles per wavefront for O^T
-  constexpr int VS = D + 2;   // V row stride in LDS (halves)
-  constexpr int PS = 64 + 8;  // P row stride in LDS (halves), keeps 16-byte row alignment
+  constexpr int KS = D / 32;      // 16x16x32 steps over d for S^T
+  constexpr int DT = D / 16;      // 16-wide d tiles of O^T (every wavefront holds all)
+  constexpr int RS = D + 4;       // V slice row stride (halves)
+  constexpr int OS = D + 4;       // merge buffer row stride (floats)
   constexpr int R = 16 * NRT;
-  _Float16* v_lds = reinterpret_cast<_Float16*>(lds);
-  _Float16* p_lds = v_lds + 64 * VS;
-  auto red = reinterpret_cast<float (*)[R]>(p_lds + R * PS);
+  constexpr int VB = 4 * 16 * RS * 2;
+  constexpr int OB = R * OS * 4;
+  constexpr int BIG = VB > OB ? VB : OB;
+  constexpr int GPR = D / 8;      // 16-byte granules per token row
+  constexpr int TPL = 64 / GPR;   // tokens per wavefront load
+  constexpr int NVL = 16 / TPL;   // V loads per lane per block
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int l16 = lane & 15, g = lane >> 4;
+  _Float16* vw = reinterpret_cast<_Float16*>(lds) + w * 16 * RS;
+  float* obuf = reinterpret_cast<float*>(lds);
+  float* mbuf = reinterpret_cast<float*>(lds + BIG);  // [4][R]
+  float* nbuf = mbuf + 4 * R;                         // [4][R]
 
   const CfSeg sg = P.segs[seg];
   const int H = P.H, C = P.C;
@@ -447,11 +573,10 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
   const int nrows = min(R, sg.row_end - rb);
   if (nrows <= 0) return;
   const int nrt = (nrows + 15) / 16;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int l16 = lane & 15, g = lane >> 4;
   const _Float16* q = static_cast<const _Float16*>(P.q);
-  const _Float16* kpool = static_cast<const _Float16*>(P.kpool);
-  const _Float16* vpool = static_cast<const _Float16*>(P.vpool);
+  const _Float16* kpool = static_cast<const _Float16*>(P.kpool) + static_cast<size_t>(h) * C * D;
+  const _Float16* vpool = static_cast<const _Float16*>(P.vpool) + static_cast<size_t>(h) * C * D;
+  const size_t slot_stride = static_cast<size_t>(H) * C * D;
 
   half8 qf[NRT][KS];
 #pragma unroll
@@ -477,129 +602,169 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
     for (int dt = 0; dt < DT; ++dt) acc[dt][t] = floatx4{0.f, 0.f, 0.f, 0.f};
   }
 
-  for (int ci = 0; ci < sg.n_chunks; ++ci) {
-    const int slot = P.seg_slots[sg.slot_off + ci];
-    const int len = P.slot_len[slot];
-    const size_t base = (static_cast<size_t>(slot) * H + h) * static_cast<size_t>(C) * D;
-    const _Float16* kb = kpool + base;
-    const _Float16* vb = vpool + base;
-    for (int t0 = 0; t0 < len; t0 += 64) {
-      const int nt = min(64, len - t0);
-      // stage V rows of this block in LDS (zeros past the valid rows)
-      constexpr int PIECES = 64 * D / 8;
+  // Segment chunks (at most 64): lane j holds chunk j's slot and length.
+  int my_slot = 0, my_len = 0;
+  if (lane < sg.n_chunks) {
+    my_slot = P.seg_slots[sg.slot_off + lane];
+    my_len = P.slot_len[my_slot];
+  }
+  int j = 0, t0 = 0;
+  int slot = __builtin_amdgcn_readlane(my_slot, 0);
+  int len = __builtin_amdgcn_readlane(my_len, 0);
+  const int ktok = 16 * w + l16;  // this lane's K row within a block
+  while (true) {
+    const int nt = min(64, len - t0);
+    const _Float16* kb = kpool + slot * slot_stride + static_cast<size_t>(t0) * D;
+    const _Float16* vb = vpool + slot * slot_stride + static_cast<size_t>(t0) * D;
+    // Unconditional loads: rows past the block's end re-read its last row
+    // (valid and finite); their scores are masked to -inf below, so P = 0.
+    half8 kf[KS];
 #pragma unroll
-      for (int pc = tid; pc < PIECES; pc += 256) {
-        const int tok = pc / (D / 8), col = (pc % (D / 8)) * 8;
-        uint4 val = make_uint4(0, 0, 0, 0);
-        if (tok < nt) val = *reinterpret_cast<const uint4*>(vb + static_cast<size_t>(t0 + tok) * D + col);
-        uint32_t* dst = reinterpret_cast<uint32_t*>(v_lds + tok * VS + col);
-        dst[0] = val.x;
-        dst[1] = val.y;
-        dst[2] = val.z;
-        dst[3] = val.w;
-      }
-      // S^T = K Q^T for this wavefront's 16 tokens
-      const int ktok = 16 * w + l16;
-      half8 kf[KS];
+    for (int s = 0; s < KS; ++s)
+      kf[s] = *reinterpret_cast<const half8*>(kb + static_cast<size_t>(min(ktok, nt - 1)) * D +
+                                              32 * s + 8 * g);
+    uint4 vr[NVL];
 #pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        if (ktok < nt)
-          kf[s] = *reinterpret_cast<const half8*>(kb + static_cast<size_t>(t0 + ktok) * D + 32 * s + 8 * g);
-        else
-          kf[s] = half8{};
+    for (int i = 0; i < NVL; ++i) {
+      const int tl = lane / GPR + TPL * i;
+      vr[i] = *reinterpret_cast<const uint4*>(vb + static_cast<size_t>(min(16 * w + tl, nt - 1)) * D +
+                                              (lane % GPR) * 8);
+    }
+    floatx4 sacc[NRT];
+#pragma unroll
+    for (int t = 0; t < NRT; ++t) {
+      sacc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
+      if (t < nrt) {
+#pragma unroll
+        for (int s = 0; s < KS; ++s)
+          sacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(kf[s], qf[t][s], sacc[t], 0, 0, 0);
       }
-      floatx4 sacc[NRT];
+    }
+    half4 ph[NRT];
+    float alpha[NRT];
+#pragma unroll
+    for (int t = 0; t < NRT; ++t) {
+      float lmax = kNegBig;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int tok = 16 * w + 4 * g + i;
+        const float x = tok < nt ? sacc[t][i] * P.qscale : -INFINITY;
+        sacc[t][i] = x;
+        lmax = fmaxf(lmax, x);
+      }
+      lmax = fmaxf(lmax, __shfl_xor(lmax, 16));
+      lmax = fmaxf(lmax, __shfl_xor(lmax, 32));
+      const float mn = fmaxf(m_run[t], lmax);
+      alpha[t] = fast_exp2(m_run[t] - mn);
+      m_run[t] = mn;
+      float ps = 0.f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        ph[t][i] = static_cast<_Float16>(fast_exp2(sacc[t][i] - mn));
+        ps += static_cast<float>(ph[t][i]);
+      }
+      n_part[t] = n_part[t] * alpha[t] + ps;
+    }
+    // this wavefront's 16 V rows -> its LDS slice (its previous reads of the
+    // slice precede these writes in program order)
+#pragma unroll
+    for (int i = 0; i < NVL; ++i) {
+      const int tl = lane / GPR + TPL * i;
+      uint2* dst = reinterpret_cast<uint2*>(vw + tl * RS + (lane % GPR) * 8);
+      dst[0] = make_uint2(vr[i].x, vr[i].y);
+      dst[1] = make_uint2(vr[i].z, vr[i].w);
+    }
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      half4 va;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) va[i] = vw[(4 * g + i) * RS + 16 * dt + l16];
 #pragma unroll
       for (int t = 0; t < NRT; ++t) {
-        sacc[t] = floatx4{0.f, 0.f, 0.f, 0.f};
         if (t < nrt) {
-#pragma unroll
-          for (int s = 0; s < KS; ++s)
-            sacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(kf[s], qf[t][s], sacc[t], 0, 0, 0);
+          acc[dt][t] *= alpha[t];
+          acc[dt][t] = __builtin_amdgcn_mfma_f32_16x16x16f16(va, ph[t], acc[dt][t], 0, 0, 0);
         }
       }
-      // lane holds S^T[token 16w+4g+i][row 16t+l16]; scale, mask, row max
-#pragma unroll
-      for (int t = 0; t < NRT; ++t) {
-        float lmax = kNegBig;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int tok = 16 * w + 4 * g + i;
-          const float x = tok < nt ? sacc[t][i] * P.qscale : -INFINITY;
-          sacc[t][i] = x;
-          lmax = fmaxf(lmax, x);
-        }
-        lmax = fmaxf(lmax, __shfl_xor(lmax, 16));
-        lmax = fmaxf(lmax, __shfl_xor(lmax, 32));
-        if (g == 0) red[w][16 * t + l16] = lmax;
-      }
-      __syncthreads();
-      float alpha[NRT];
-#pragma unroll
-      for (int t = 0; t < NRT; ++t) {
-        const int r = 16 * t + l16;
-        const float bmax = fmaxf(fmaxf(red[0][r], red[1][r]), fmaxf(red[2][r], red[3][r]));
-        const float mn = fmaxf(m_run[t], bmax);
-        alpha[t] = fast_exp2(m_run[t] - mn);
-        m_run[t] = mn;
-        half4 ph;
-        float ps = 0.f;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          ph[i] = static_cast<_Float16>(fast_exp2(sacc[t][i] - mn));
-          ps += static_cast<float>(ph[i]);
-        }
-        n_part[t] = n_part[t] * alpha[t] + ps;
-        *reinterpret_cast<half4*>(p_lds + r * PS + 16 * w + 4 * g) = ph;
-      }
-      __syncthreads();
-      // O^T += V^T P^T over the block's 64 tokens (two k-steps of 32)
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        const int d0 = w * (D / 4) + 16 * dt;
-#pragma unroll
-        for (int t = 0; t < NRT; ++t) acc[dt][t] *= alpha[t];
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-          half8 va;
-#pragma unroll
-          for (int j = 0; j < 8; ++j) va[j] = v_lds[(32 * ks + 8 * g + j) * VS + d0 + l16];
-#pragma unroll
-          for (int t = 0; t < NRT; ++t) {
-            if (t < nrt) {
-              const half8 pb =
-                  *reinterpret_cast<const half8*>(p_lds + (16 * t + l16) * PS + 32 * ks + 8 * g);
-              acc[dt][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(va, pb, acc[dt][t], 0, 0, 0);
-            }
-          }
-        }
-      }
-      __syncthreads();
+    }
+    // next block
+    t0 += 64;
+    if (t0 >= len) {
+      t0 = 0;
+      ++j;
+      if (j >= sg.n_chunks) break;
+      slot = __builtin_amdgcn_readlane(my_slot, j);
+      len = __builtin_amdgcn_readlane(my_len, j);
     }
   }
 
-  // row sums: combine lane groups and wavefronts
+  // Merge the four wavefront states per row: common max, rescaled sums.
+  float nw[NRT];
 #pragma unroll
   for (int t = 0; t < NRT; ++t) {
     float ns = n_part[t];
     ns += __shfl_xor(ns, 16);
     ns += __shfl_xor(ns, 32);
-    if (g == 0) red[w][16 * t + l16] = ns;
+    nw[t] = ns;
+    if (g == 0) {
+      mbuf[w * R + 16 * t + l16] = m_run[t];
+      nbuf[w * R + 16 * t + l16] = ns;
+    }
   }
-  __syncthreads();
+  __syncthreads();  // all wavefronts are past their loops: the slices are free
+  float scale[NRT], Mrow[NRT], Nrow[NRT];
 #pragma unroll
   for (int t = 0; t < NRT; ++t) {
     const int r = 16 * t + l16;
-    if (r < nrows) {
-      const size_t p = static_cast<size_t>(sg.part_base + (rb - sg.row_begin) + r);
-      float* po = P.ws_o + (p * H + h) * D;
+    float M = kNegBig;
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
-        *reinterpret_cast<floatx4*>(po + w * (D / 4) + 16 * dt + 4 * g) = acc[dt][t];
-      if (w == 0 && g == 0)
-        P.ws_ml[p * H + h] = make_float2(m_run[t], red[0][r] + red[1][r] + red[2][r] + red[3][r]);
+    for (int ww = 0; ww < 4; ++ww) M = fmaxf(M, mbuf[ww * R + r]);
+    float N = 0.f;
+#pragma unroll
+    for (int ww = 0; ww < 4; ++ww) N += nbuf[ww * R + r] * fast_exp2(mbuf[ww * R + r] - M);
+    scale[t] = fast_exp2(m_run[t] - M);
+    Mrow[t] = M;
+    Nrow[t] = N;
+    (void)nw[t];
+  }
+  for (int ww = 0; ww < 4; ++ww) {
+    if (w == ww) {
+#pragma unroll
+      for (int t = 0; t < NRT; ++t) {
+        if (t < nrt) {
+          const int r = 16 * t + l16;
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              float* dst = obuf + r * OS + 16 * dt + 4 * g + i;
+              const float v = acc[dt][t][i] * scale[t];
+              *dst = ww == 0 ? v : *dst + v;
+            }
+          }
+        }
+      }
+    }
+    __syncthreads();
+  }
+  // write the segment's partial (O, m, n) for every covered row
+  const size_t pbase = static_cast<size_t>(sg.part_base + (rb - sg.row_begin));
+  for (int e = tid; e < nrows * D; e += 256) {
+    const int r = e / D, d = e % D;
+    st_dev(P.ws_o + ((pbase + r) * H + h) * D + d, obuf[r * OS + d]);
+  }
+  if (w == 0 && g == 0) {
+#pragma unroll
+    for (int t = 0; t < NRT; ++t) {
+      const int r = 16 * t + l16;
+      if (r < nrows) {
+        float* pml = reinterpret_cast<float*>(P.ws_ml + (pbase + r) * H + h);
+        st_dev(pml, Mrow[t]);
+        st_dev(pml + 1, Nrow[t]);
+      }
     }
   }
+  if (P.cnt) cf_arrive<OUT_T, D, R>(P, rb, nrows, h, reinterpret_cast<float (*)[R]>(mbuf));
 }
 
 // fp32 chunk-first: the same schedule on the 16x16x4 fp32 matrix-core op.
@@ -609,7 +774,7 @@ constexpr int kcf_f32_lds_bytes() {
   return 64 * (D + 1) * 4 + 16 * NRT * (64 + 1) * 4 + 4 * 16 * NRT * 4;
 }
 
-template <int D, int NRT>
+template <int D, int NRT, typename OUT_T = float>
 __device__ __forceinline__ void kcf_f32_block(const KcfParams& P, int seg, int z, int h, char* lds) {
   constexpr int DT = D / 64;
   constexpr int VS = D + 1;
@@ -743,12 +908,18 @@ __device__ __forceinline__ void kcf_f32_block(const KcfParams& P, int seg, int z
       const size_t p = static_cast<size_t>(sg.part_base + (rb - sg.row_begin) + r);
       float* po = P.ws_o + (p * H + h) * D;
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
-        *reinterpret_cast<floatx4*>(po + w * (D / 4) + 16 * dt + 4 * g) = acc[dt][t];
-      if (w == 0 && g == 0)
-        P.ws_ml[p * H + h] = make_float2(m_run[t], red[0][r] + red[1][r] + red[2][r] + red[3][r]);
+      for (int dt = 0; dt < DT; ++dt) {
+        const floatx4 v = acc[dt][t];
+        st_dev4(po + w * (D / 4) + 16 * dt + 4 * g, v[0], v[1], v[2], v[3]);
+      }
+      if (w == 0 && g == 0) {
+        float* pml = reinterpret_cast<float*>(P.ws_ml + p * H + h);
+        st_dev(pml, m_run[t]);
+        st_dev(pml + 1, red[0][r] + red[1][r] + red[2][r] + red[3][r]);
+      }
     }
   }
+  if (P.cnt) cf_arrive<OUT_T, D, R>(P, rb, nrows, h, red);
 }
 
 // ---------------------------------------------------------------------------
@@ -792,12 +963,15 @@ __global__ __launch_bounds__(256) void kkv_kernel(KvJobBatch b, const char* k, c
   if (h == 0 && threadIdx.x == 0) slot_len[j.dst_slot] = j.kind == 2 ? j.dst_pos : j.dst_pos + j.n;
 }
 
-// Fused schedule, one launch for both phases: blocks [0, n_cf) run
-// chunk-first work items (dispatched first), the remaining blocks run
-// sequence-first items; both write partial results and the merge epilogue
-// combines them. Sequential schedule: chunk-first launch, then a
-// sequence-first launch whose items fold the finished chunk-first partials
-// themselves (the merge epilogue only finishes split rows).
+// Schedules. 0 sequential: chunk-first launch, then a sequence-first launch
+// whose items fold the finished chunk-first partials themselves (the merge
+// epilogue only finishes split rows). 1 fused: one launch, blocks [0, n_cf)
+// run chunk-first items (dispatched first), the rest sequence-first items;
+// every item writes a partial and the merge epilogue finishes the rows.
+// 2 fused with in-kernel merge: as 1, but every item counts its arrival on
+// its rows and the last contributor of a row finishes it. 3 concurrent: the
+// chunk-first kernel on a side stream, the sequence-first kernel on the
+// caller's stream at the same time, rows finished as in 2.
 struct TppParams {
   KcfParams cf;
   KsfParams sf;
@@ -855,33 +1029,70 @@ __global__ __launch_bounds__(256) void ksf_kernel(KsfParams P) {
 }
 
 template <typename T, int D, int NRT>
-void launch_phases(const TppParams& P, int n_sf, bool fused, int mask, hipStream_t s) {
-  if (fused && (mask & 1) && (mask & 2)) {
+hipError_t launch_phases(const TppParams& P, int n_sf, int schedule, int mask, hipStream_t s,
+                         const SideStream& side) {
+  const bool both = (mask & 3) == 3;
+  if ((schedule == 1 || schedule == 2) && both) {
     const int grid = P.n_cf + n_sf;
     if (grid > 0) tpp_kernel<T, D, NRT><<<grid, 256, 0, s>>>(P);
-    return;
+    return hipSuccess;
   }
-  if ((mask & 1) && P.n_cf > 0) kcf_kernel<T, D, NRT><<<P.n_cf, 256, 0, s>>>(P.cf, P.zb);
-  if ((mask & 2) && n_sf > 0) ksf_kernel<T, D><<<n_sf, 256, 0, s>>>(P.sf);
+  if (schedule == 3 && both && P.n_cf > 0 && n_sf > 0) {
+    // chunk-first on the side stream, sequence-first on the caller's stream,
+    // concurrently; the caller's stream then waits for the side stream
+    hipError_t e;
+    if ((e = hipEventRecord(side.fork, s)) != hipSuccess) return e;
+    if ((e = hipStreamWaitEvent(side.stream, side.fork, 0)) != hipSuccess) return e;
+    kcf_kernel<T, D, NRT><<<P.n_cf, 256, 0, side.stream>>>(P.cf, P.zb);
+    if ((e = hipEventRecord(side.join, side.stream)) != hipSuccess) return e;
+    ksf_kernel<T, D><<<n_sf, 256, 0, s>>>(P.sf);
+    return hipStreamWaitEvent(s, side.join, 0);
+  }
+  // phases one after another on the caller's stream; arrival counting only
+  // when this is the complete attention of a counting schedule
+  KcfParams cf = P.cf;
+  KsfParams sf = P.sf;
+  if (!both) {
+    cf.cnt = nullptr;
+    sf.cnt = nullptr;
+  }
+  if ((mask & 1) && P.n_cf > 0) kcf_kernel<T, D, NRT><<<P.n_cf, 256, 0, s>>>(cf, P.zb);
+  if ((mask & 2) && n_sf > 0) ksf_kernel<T, D><<<n_sf, 256, 0, s>>>(sf);
+  return hipSuccess;
 }
 
 template <typename T, int D>
-hipError_t launch_all(const AttnArgs& a, const DevWork& w, hipStream_t s, int mask) {
+hipError_t launch_all(const AttnArgs& a, const DevWork& w, hipStream_t s, int mask,
+                      const SideStream& side) {
   TppParams P;
+  const bool counting = w.schedule >= 2;  // the last contributor finishes each row
   P.cf = KcfParams{a.q, a.kpool, a.vpool, a.slot_len, w.segs, w.seg_slots, a.ws_o,
-                   reinterpret_cast<float2*>(a.ws_ml), a.H, a.C, a.qscale};
+                   reinterpret_cast<float2*>(a.ws_ml), a.H, a.C, a.qscale,
+                   counting ? a.cnt : nullptr, a.o, w.part_ptr, w.parts};
   P.sf = KsfParams{a.q, a.o, a.kpool, a.vpool, a.slot_len, w.items, w.priv_slot, w.part_ptr,
-                   w.parts, a.ws_o, reinterpret_cast<float2*>(a.ws_ml), a.H, a.C, a.qscale};
+                   w.parts, a.ws_o, reinterpret_cast<float2*>(a.ws_ml), a.H, a.C, a.qscale,
+                   counting ? a.cnt : nullptr};
+  // At most 16 or 32 covered rows per chunk-first block; wider runs take
+  // several row blocks, which re-read the chunk. Their block indices differ
+  // by a multiple of H, so for H a multiple of 8 they land on the same XCD
+  // (blocks go to XCDs round-robin) and the re-reads hit that XCD's L2.
+  // The fused launch carries the chunk-first path's registers into every
+  // block, so there chunk-first blocks take 16 rows; alone they take 32.
   const int rows = w.max_seg_rows;
-  const int nrt = rows <= 16 ? 1 : rows <= 32 ? 2 : 4;
+  const bool fused = (w.schedule == 1 || w.schedule == 2) && (mask & 3) == 3;
+  const int nrt = rows <= 16 || fused ? 1 : 2;
   P.zb = rows > 0 ? (rows + 16 * nrt - 1) / (16 * nrt) : 1;
   P.n_cf = w.n_segs * P.zb * a.H;
   P.block_base = 0;
   const int n_sf = w.n_items * a.H;
-  if (nrt == 1) launch_phases<T, D, 1>(P, n_sf, w.fused, mask, s);
-  else if (nrt == 2) launch_phases<T, D, 2>(P, n_sf, w.fused, mask, s);
-  else launch_phases<T, D, 4>(P, n_sf, w.fused, mask, s);
-  if ((mask & 4) && w.n_mg > 0) {
+  hipError_t e;
+  if (nrt == 1) e = launch_phases<T, D, 1>(P, n_sf, w.schedule, mask, s, side);
+  else e = launch_phases<T, D, 2>(P, n_sf, w.schedule, mask, s, side);
+  if (e != hipSuccess) return e;
+  // Partial-writing schedules finish their rows inside the kernels; the merge
+  // epilogue runs in the sequential schedule (split rows) or on its own.
+  const bool self_finished = counting && (mask & 3) == 3;
+  if ((mask & 4) && w.n_mg > 0 && !self_finished) {
     KmgParams M{a.o, w.mg_rows, w.part_ptr, w.parts, a.ws_o, reinterpret_cast<const float2*>(a.ws_ml),
                 a.H};
     kmg_kernel<T, D><<<dim3(w.n_mg, a.H), 64, 0, s>>>(M);
@@ -891,13 +1102,14 @@ hipError_t launch_all(const AttnArgs& a, const DevWork& w, hipStream_t s, int ma
 
 }  // namespace
 
-hipError_t launch_attention(const AttnArgs& a, const DevWork& w, hipStream_t s, int mask) {
+hipError_t launch_attention(const AttnArgs& a, const DevWork& w, hipStream_t s, int mask,
+                            const SideStream& side) {
   if (a.dtype == 0) {
-    if (a.D == 128) return launch_all<_Float16, 128>(a, w, s, mask);
-    if (a.D == 64) return launch_all<_Float16, 64>(a, w, s, mask);
+    if (a.D == 128) return launch_all<_Float16, 128>(a, w, s, mask, side);
+    if (a.D == 64) return launch_all<_Float16, 64>(a, w, s, mask, side);
   } else {
-    if (a.D == 128) return launch_all<float, 128>(a, w, s, mask);
-    if (a.D == 64) return launch_all<float, 64>(a, w, s, mask);
+    if (a.D == 128) return launch_all<float, 128>(a, w, s, mask, side);
+    if (a.D == 64) return launch_all<float, 64>(a, w, s, mask, side);
   }
   return hipErrorInvalidValue;
 }

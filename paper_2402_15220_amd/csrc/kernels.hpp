@@ -23,7 +23,15 @@ struct DevWork {
   const int32_t* parts = nullptr;
   const int32_t* mg_rows = nullptr;
   int32_t n_mg = 0;
-  bool fused = false;  // one launch for both phases (items then never own a shared row)
+  int schedule = 0;  // 0 sequential, 1 fused + merge epilogue, 2 fused + in-kernel merge,
+                     // 3 concurrent streams + in-kernel merge
+};
+
+// Second stream and events for the concurrent schedule (default priority).
+struct SideStream {
+  hipStream_t stream = nullptr;
+  hipEvent_t fork = nullptr;
+  hipEvent_t join = nullptr;
 };
 
 struct AttnArgs {
@@ -37,12 +45,14 @@ struct AttnArgs {
   float* ws_o;   // [n_parts][H][D]
   float* ws_ml;  // [n_parts][H][2] (running max in log2 units, sum)
   float qscale;  // softmax scale * log2(e)
+  int32_t* cnt;  // [B][H] arrival counters, zero between launches
 };
 
-// Enqueue the chunk-first, sequence-first and merge kernels. `phase_mask`
-// selects phases (bit 0 chunk-first, bit 1 sequence-first, bit 2 merge).
+// Enqueue the attention kernels. `phase_mask` selects phases (bit 0
+// chunk-first, bit 1 sequence-first, bit 2 merge). In the fused and
+// concurrent schedules bits 0 and 1 together also finish every row.
 hipError_t launch_attention(const AttnArgs& a, const DevWork& w, hipStream_t stream,
-                            int phase_mask = 7);
+                            int phase_mask, const SideStream& side);
 
 // K/V row copies for tree operations (at most kKvJobsPerLaunch per call).
 constexpr int kKvJobsPerLaunch = 64;

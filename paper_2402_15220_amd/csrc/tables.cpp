@@ -105,11 +105,10 @@ void build_tables(const ChunkTree& tree, Tables* out) {
 }
 
 void build_work(const ChunkTree& tree, const Tables& T, int32_t seg_chunks, int32_t split_chunks,
-                bool fused, WorkLists* out) {
+                bool partial_items, int32_t num_heads, int32_t num_cus, WorkLists* out) {
   WorkLists& W = *out;
   const int64_t B = static_cast<int64_t>(T.row_seq.size());
   const size_t nn = T.node_slot.size();
-  if (seg_chunks < 1) seg_chunks = 1;
 
   // Runs: a shared node continues its parent's run when the parent is shared
   // and covers the same rows (BFS order visits parents first).
@@ -126,6 +125,21 @@ void build_work(const ChunkTree& tree, const Tables& T, int32_t seg_chunks, int3
     }
     runs[run_of[i]].push_back(i);
   }
+
+  // Automatic segment size: about one chunk-first block per compute unit,
+  // counting a run of L chunks over r rows as L * ceil(r/16) * H chunk-blocks
+  // (16 rows per block in the fused launch); at most 16 chunks per segment.
+  if (seg_chunks <= 0) {
+    int64_t work = 0;
+    for (const auto& chain : runs) {
+      const int64_t r = T.node_row_end[chain[0]] - T.node_row_begin[chain[0]];
+      work += static_cast<int64_t>(chain.size()) * ((r + 15) / 16) * num_heads;
+    }
+    const int64_t cus = num_cus > 0 ? num_cus : 256;
+    seg_chunks = static_cast<int32_t>(std::min<int64_t>(16, std::max<int64_t>(1, (work + cus - 1) / cus)));
+  }
+  if (seg_chunks > 64) seg_chunks = 64;  // the chunk-first kernel keeps a segment's slots in lanes
+  W.seg_chunks = seg_chunks;
 
   W.segs.clear();
   W.seg_slots.clear();
@@ -175,7 +189,7 @@ void build_work(const ChunkTree& tree, const Tables& T, int32_t seg_chunks, int3
     const int32_t pe = static_cast<int32_t>(W.priv_slot.size());
     const int32_t np = pe - pb;
     const bool has_shared = static_cast<int32_t>(W.parts.size()) > W.part_ptr.back();
-    if (!(fused && has_shared) && (split_chunks <= 0 || np <= split_chunks)) {
+    if (!(partial_items && has_shared) && (split_chunks <= 0 || np <= split_chunks)) {
       // the row's own item produces its output directly
       W.items.push_back({static_cast<int32_t>(r), pb, pe, -1});
     } else {

@@ -34,10 +34,14 @@ void build_tables(const ChunkTree& tree, Tables* out);
 //  * Each row's private chunks form one sequence-first item, or several of
 //    at most split_chunks chunks (split_chunks <= 0 disables splitting).
 //    An unsplit row is finished by its item (o written directly), which in
-//    the sequential schedule also folds the row's chunk-first partials. In
-//    the fused schedule the chunk-first items run concurrently, so a row with
-//    shared chunks has its item write a partial and the merge epilogue
-//    (mg_rows) finishes it; split rows are always finished by the epilogue.
+//    the sequential schedule also folds the row's chunk-first partials. With
+//    partial_items (schedules where the chunk-first items run at the same
+//    time), a row with shared chunks has its item write a partial and the
+//    row's last contributor finishes it; split rows always write partials.
+//    mg_rows lists the rows finished from partials.
+//  * seg_chunks <= 0 picks the size automatically (about one chunk-first
+//    block per compute unit, at most 16 chunks); explicit sizes are clamped
+//    to 64.
 //  * part lists per row: the row's segment partials root -> leaf, then its
 //    sequence-first partials in chunk order.
 struct WorkLists {
@@ -50,9 +54,10 @@ struct WorkLists {
   std::vector<int32_t> mg_rows;    // rows whose result the merge kernel writes
   int64_t n_parts = 0;
   int32_t max_seg_rows = 0;
+  int32_t seg_chunks = 0;  // segment size used
 };
 
 void build_work(const ChunkTree& tree, const Tables& t, int32_t seg_chunks, int32_t split_chunks,
-                bool fused, WorkLists* out);
+                bool partial_items, int32_t num_heads, int32_t num_cus, WorkLists* out);
 
 }  // namespace ca

@@ -47,17 +47,20 @@ def test_static_config(cfg):
     assert_close(o, ref, wl.dtype, f"config {cfg} (B={tb['row_seq'].shape[0]})")
 
 
-@pytest.mark.parametrize("seg,split,fused", [(1, 0, 0), (16, 0, 0), (4, 3, 0), (2, 1, 0), (64, 5, 0),
-                                             (1, 0, 1), (4, 0, 1), (16, 3, 1), (3, 1, 1)])
-def test_config2_work_partitions(seg, split, fused):
-    """Every schedule, segment size and split gives the same result."""
-    print(f"[case] config 2 seg={seg} split={split} fused={fused}", flush=True)
+@pytest.mark.parametrize("seg,split,sched", [(1, 0, 0), (16, 0, 0), (4, 3, 0), (2, 1, 0), (64, 5, 0),
+                                             (1, 0, 1), (4, 0, 1), (16, 3, 1), (3, 1, 1),
+                                             (1, 0, 2), (8, 0, 2), (16, 2, 2), (64, 1, 2), (4, 0, 3), (16, 3, 3)])
+def test_config2_work_partitions(seg, split, sched):
+    """Every schedule, segment size and split gives the same result, and
+    repeated calls (counters reset by the kernels) stay correct."""
+    print(f"[case] config 2 seg={seg} split={split} schedule={sched}", flush=True)
     wl = make_static(2)
     p = _static_pair(wl)
-    p.cache.set_tuning(seg_chunks=seg, split_chunks=split, fused=fused)
-    o, q, row_seq = p.attention({s.seq_id: wl.q[s.seq_id] for s in wl.seqs})
-    ref = p.reference(row_seq, q, 0.0)
-    assert_close(o, ref, wl.dtype, f"config 2 seg={seg} split={split} fused={fused}")
+    p.cache.set_tuning(seg_chunks=seg, split_chunks=split, schedule=sched)
+    for rep in range(3):
+        o, q, row_seq = p.attention({s.seq_id: wl.q[s.seq_id] for s in wl.seqs})
+        ref = p.reference(row_seq, q, 0.0) if rep == 0 else ref
+        assert_close(o, ref, wl.dtype, f"config 2 seg={seg} split={split} schedule={sched} rep={rep}")
 
 
 @pytest.mark.timeout(900)
