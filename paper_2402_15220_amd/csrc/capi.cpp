@@ -456,7 +456,12 @@ ca_status ca_attention(ca_cache* cache, const void* q, void* o, float scale, voi
   a.vpool = cache->cfg.v_pool;
   a.slot_len = cache->d_slot_len;
   const size_t np = static_cast<size_t>(cache->work.n_parts);
+  const size_t o_bytes = np * a.H * a.D * 4;
+  if (o_bytes > 0xFFFFFFFFull)
+    return fail(CA_ERR_INVALID, "ca_attention: partial-O workspace above 4 GiB (" +
+                                    std::to_string(o_bytes) + " bytes); use longer segments");
   a.ws_o = static_cast<float*>(ws);
+  a.ws_o_bytes = static_cast<uint32_t>(o_bytes);
   a.ws_ml = np ? reinterpret_cast<float*>(static_cast<char*>(ws) +
                                           align_up(np * a.H * a.D * 4, 256))
                : nullptr;

@@ -127,36 +127,70 @@ __device__ __forceinline__ float readlane_f(float x, int l) {
 // XCDs, each with its own L2) with device-scope stores and loads (`sc1`):
 // they are coherent across XCDs per instruction, so no whole-cache writeback
 // or invalidate is needed. A writer waits for its stores to complete
-// (vmcnt(0)) before counting its arrival.
+// (vmcnt(0)) before counting its arrival. Partial O vectors move as 16-byte
+// raw buffer accesses over the partial-O workspace (descriptor word 3 is the
+// gfx9 raw-buffer format; byte offsets are 32-bit, the host keeps that
+// region below 4 GiB).
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+constexpr int kRsrcWord3 = 0x00020000;
+constexpr int kDevScope = 16;  // cache-policy bit sc1
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t part_rsrc(const float* ws_o, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(ws_o), 0, static_cast<int>(bytes),
+                                           kRsrcWord3);
+}
+__device__ __forceinline__ float4 ld_dev4(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<int>(off), 0, kDevScope);
+  return make_float4(__uint_as_float(v.x), __uint_as_float(v.y), __uint_as_float(v.z),
+                     __uint_as_float(v.w));
+}
+__device__ __forceinline__ void st_dev4(__amdgpu_buffer_rsrc_t r, uint32_t off, float a, float b,
+                                        float c, float d) {
+  const u32x4 v = {__float_as_uint(a), __float_as_uint(b), __float_as_uint(c), __float_as_uint(d)};
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, static_cast<int>(off), 0, kDevScope);
+}
 __device__ __forceinline__ void st_dev(float* p, float x) {
   __hip_atomic_store(p, x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void st_dev4(float* p, float a, float b, float c, float d) {
-  st_dev(p, a);
-  st_dev(p + 1, b);
-  st_dev(p + 2, c);
-  st_dev(p + 3, d);
 }
 __device__ __forceinline__ float ld_dev(const float* p) {
   return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ void wait_stores() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
 
+// Byte offset of element d of partial p, head h in the partial-O workspace.
+__device__ __forceinline__ uint32_t part_off(int p, int H, int D, int h, int d) {
+  return ((static_cast<uint32_t>(p) * H + h) * D + d) * 4u;
+}
+
 // attn_reduce (Eqn 2) of partials parts[k0..k1) into (m, n, acc), a whole
-// wavefront cooperating: the lanes read up to 64 partial maxima at once, the
-// common maximum rescales everything once, then every lane accumulates its
-// d-slice [d0, d0+E) of each partial's O (independent loads, in flight
-// together). Call with all 64 lanes active.
-template <int E, bool DEV>
+// wavefront cooperating. The lanes read up to 64 partial maxima at once and
+// one common maximum rescales everything once. The wavefront is G groups of
+// 64/G lanes; each lane owns the d-slice [d0, d0+E) and its group takes
+// every G-th partial, all loads of a batch (NB partials per group) issued
+// before the first is used; the group sums are added at the end, so every
+// lane returns the whole result for its slice. (m, n, acc) must be the same
+// in every group on entry. A skipped partial (`skip`, this block's own) or
+// an absent one gets weight 0 and reads a valid partial in its place, never
+// unwritten workspace. DEV selects device-scope loads (partials written by
+// other blocks of the same launch). Call with all 64 lanes active.
+template <int E, int G, bool DEV>
 __device__ __forceinline__ void fold_parts(int k0, int k1, const int32_t* parts, const float* ws_o,
-                                           const float2* ws_ml, int H, int D, int h, int d0,
-                                           int lane, float& m, float& n, float* acc, int skip = -1) {
+                                           uint32_t o_bytes, const float2* ws_ml, int H, int D,
+                                           int h, int d0, int lane, float& m, float& n, float* acc,
+                                           int skip = -1) {
+  constexpr int NB = 32 / E;
+  static_assert(E % 4 == 0 && NB >= 1 && G >= 1 && 64 % G == 0, "fold layout");
+  const int gi = lane / (64 / G);
+  const __amdgpu_buffer_rsrc_t rs = part_rsrc(ws_o, o_bytes);
+  if (gi != 0) {
+#pragma unroll
+    for (int j = 0; j < E; ++j) acc[j] = 0.f;
+  }
   for (int b0 = k0; b0 < k1; b0 += 64) {
     const int nb = min(64, k1 - b0);
-    int pidx = 0;
+    int pidx = lane < nb ? parts[b0 + lane] : -1;
+    const bool valid = pidx >= 0 && pidx != skip;
     float pm = kNegBig, pn = 0.f;
-    if (lane < nb && parts[b0 + lane] != skip) {
-      pidx = parts[b0 + lane];
+    if (valid) {
       const float* ml = reinterpret_cast<const float*>(ws_ml + static_cast<size_t>(pidx) * H + h);
       if constexpr (DEV) {
         pm = ld_dev(ml);
@@ -166,33 +200,51 @@ __device__ __forceinline__ void fold_parts(int k0, int k1, const int32_t* parts,
         pn = ml[1];
       }
     }
+    const unsigned long long vm = __ballot(valid);
+    if (vm == 0) continue;  // uniform
+    if (!valid) pidx = __builtin_amdgcn_readlane(pidx, __builtin_ctzll(vm));
     const float M = fmaxf(m, wave_max(pm));
     const float wself = fast_exp2(m - M);
-    const float wp = lane < nb ? fast_exp2(pm - M) : 0.f;
+    const float wp = valid ? fast_exp2(pm - M) : 0.f;
     n = n * wself + wave_sum(wp * pn);
 #pragma unroll
     for (int j = 0; j < E; ++j) acc[j] *= wself;
-#pragma unroll 4
-    for (int k = 0; k < nb; ++k) {
-      if (parts[b0 + k] == skip) continue;  // uniform
-      const int pk = __builtin_amdgcn_readlane(pidx, k);
-      const float wk = readlane_f(wp, k);
-      const float* po = ws_o + (static_cast<size_t>(pk) * H + h) * D + d0;
+    const int kend = 64 - __builtin_clzll(vm);  // one past the last valid lane
+    for (int kb = 0; kb < kend; kb += NB * G) {
+      float x[NB][E];
+      float wk[NB];
 #pragma unroll
-      for (int j = 0; j < E; j += 4) {
-        float4 x;
-        if constexpr (DEV) {
-          x = make_float4(ld_dev(po + j), ld_dev(po + j + 1), ld_dev(po + j + 2), ld_dev(po + j + 3));
-        } else {
-          x = *reinterpret_cast<const float4*>(po + j);
+      for (int u = 0; u < NB; ++u) {
+        const int k = kb + G * u + gi;
+        const int kc = min(k, 63);
+        const int pk = __shfl(pidx, kc);
+        wk[u] = k < 64 ? __shfl(wp, kc) : 0.f;
+#pragma unroll
+        for (int j = 0; j < E; j += 4) {
+          float4 v;
+          if constexpr (DEV) {
+            v = ld_dev4(rs, part_off(pk, H, D, h, d0 + j));
+          } else {
+            v = *reinterpret_cast<const float4*>(ws_o + (static_cast<size_t>(pk) * H + h) * D + d0 + j);
+          }
+          x[u][j] = v.x;
+          x[u][j + 1] = v.y;
+          x[u][j + 2] = v.z;
+          x[u][j + 3] = v.w;
         }
-        acc[j] = fmaf(wk, x.x, acc[j]);
-        acc[j + 1] = fmaf(wk, x.y, acc[j + 1]);
-        acc[j + 2] = fmaf(wk, x.z, acc[j + 2]);
-        acc[j + 3] = fmaf(wk, x.w, acc[j + 3]);
+      }
+#pragma unroll
+      for (int u = 0; u < NB; ++u) {
+#pragma unroll
+        for (int j = 0; j < E; ++j) acc[j] = fmaf(wk[u], x[u][j], acc[j]);
       }
     }
     m = M;
+  }
+#pragma unroll
+  for (int j = 0; j < E; ++j) {
+#pragma unroll
+    for (int off = 64 / G; off < 64; off <<= 1) acc[j] += __shfl_xor(acc[j], off);
   }
 }
 
@@ -201,12 +253,12 @@ __device__ __forceinline__ void fold_parts(int k0, int k1, const int32_t* parts,
 // device-scope loads (partials written by other blocks of the same launch).
 template <typename T, int D, bool DEV>
 __device__ __forceinline__ void finish_row(const int32_t* part_ptr, const int32_t* parts,
-                                           const float* ws_o, const float2* ws_ml, void* o, int H,
-                                           int row, int h, int lane) {
+                                           const float* ws_o, uint32_t o_bytes, const float2* ws_ml,
+                                           void* o, int H, int row, int h, int lane) {
   const int d0 = (lane % (D / 4)) * 4;
   float m = kNegBig, n = 0.f, acc[4] = {0.f, 0.f, 0.f, 0.f};
-  fold_parts<4, DEV>(part_ptr[row], part_ptr[row + 1], parts, ws_o, ws_ml, H, D, h, d0, lane, m, n,
-                     acc);
+  fold_parts<4, 256 / D, DEV>(part_ptr[row], part_ptr[row + 1], parts, ws_o, o_bytes, ws_ml, H, D,
+                              h, d0, lane, m, n, acc);
   if (lane < D / 4) {
     const float inv = 1.f / n;
     T* out = static_cast<T*>(o) + (static_cast<size_t>(row) * H + h) * D + d0;
@@ -242,6 +294,7 @@ struct KsfParams {
   const int32_t* parts;
   float* ws_o;
   float2* ws_ml;
+  uint32_t o_bytes;  // bytes of the partial-O region at ws_o
   int H;
   int C;
   float qscale;
@@ -388,8 +441,8 @@ __device__ __forceinline__ void ksf_block(const KsfParams& P, int item, int h, c
 
   if (it.out_part < 0) {
     // fold the row's chunk-first partials (Algorithm 2), then O/n
-    fold_parts<EPL, false>(P.part_ptr[it.row], P.part_ptr[it.row + 1], P.parts, P.ws_o, P.ws_ml, H,
-                           D, h, sub * EPL, lane, m, n, acc);
+    fold_parts<EPL, 64 / LPT, false>(P.part_ptr[it.row], P.part_ptr[it.row + 1], P.parts, P.ws_o,
+                                     P.o_bytes, P.ws_ml, H, D, h, sub * EPL, lane, m, n, acc);
     if (tr != 0) return;
     const float inv = 1.f / n;
 #pragma unroll
@@ -409,8 +462,8 @@ __device__ __forceinline__ void ksf_block(const KsfParams& P, int item, int h, c
         ready = __hip_atomic_load(c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == k1 - k0 - 1;
       if (__shfl(ready, 0)) {
         __atomic_signal_fence(__ATOMIC_SEQ_CST);
-        fold_parts<EPL, true>(k0, k1, P.parts, P.ws_o, P.ws_ml, H, D, h, sub * EPL, lane, m, n, acc,
-                              it.out_part);
+        fold_parts<EPL, 64 / LPT, true>(k0, k1, P.parts, P.ws_o, P.o_bytes, P.ws_ml, H, D, h,
+                                        sub * EPL, lane, m, n, acc, it.out_part);
         if (lane == 0) __hip_atomic_store(c, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (tr != 0) return;
         const float inv = 1.f / n;
@@ -422,9 +475,11 @@ __device__ __forceinline__ void ksf_block(const KsfParams& P, int item, int h, c
       }
     }
     if (tr == 0) {
-      float* po = P.ws_o + (static_cast<size_t>(it.out_part) * H + h) * D + sub * EPL;
+      const __amdgpu_buffer_rsrc_t rs = part_rsrc(P.ws_o, P.o_bytes);
 #pragma unroll
-      for (int j = 0; j < EPL; j += 4) st_dev4(po + j, acc[j], acc[j + 1], acc[j + 2], acc[j + 3]);
+      for (int j = 0; j < EPL; j += 4)
+        st_dev4(rs, part_off(it.out_part, H, D, h, sub * EPL + j), acc[j], acc[j + 1], acc[j + 2],
+                acc[j + 3]);
       if (sub == 0) {
         float* pml = reinterpret_cast<float*>(P.ws_ml + static_cast<size_t>(it.out_part) * H + h);
         st_dev(pml, m);
@@ -440,7 +495,8 @@ __device__ __forceinline__ void ksf_block(const KsfParams& P, int item, int h, c
         last = arrive_last(P.cnt + static_cast<size_t>(it.row) * H + h, need);
       }
       if (__shfl(last, 0))
-        finish_row<T, D, true>(P.part_ptr, P.parts, P.ws_o, P.ws_ml, P.o, H, it.row, h, lane);
+        finish_row<T, D, true>(P.part_ptr, P.parts, P.ws_o, P.o_bytes, P.ws_ml, P.o, H, it.row, h,
+                               lane);
     }
   }
 }
@@ -455,12 +511,14 @@ struct KmgParams {
   const int32_t* parts;
   const float* ws_o;
   const float2* ws_ml;
+  uint32_t o_bytes;
   int H;
 };
 
 template <typename T, int D>
 __global__ __launch_bounds__(64) void kmg_kernel(KmgParams P) {
-  finish_row<T, D, false>(P.part_ptr, P.parts, P.ws_o, P.ws_ml, P.o, P.H, P.mg_rows[blockIdx.x],
+  finish_row<T, D, false>(P.part_ptr, P.parts, P.ws_o, P.o_bytes, P.ws_ml, P.o, P.H,
+                          P.mg_rows[blockIdx.x],
                           blockIdx.y, threadIdx.x);
 }
 
@@ -476,6 +534,7 @@ struct KcfParams {
   const int32_t* seg_slots;
   float* ws_o;
   float2* ws_ml;
+  uint32_t o_bytes;  // bytes of the partial-O region at ws_o
   int H;
   int C;
   float qscale;
@@ -512,7 +571,8 @@ __device__ __forceinline__ void cf_arrive(const KcfParams& P, int rb, int nrows,
   if (!any) return;
   for (int r = w; r < nrows; r += 4)
     if (flags[r])
-      finish_row<T, D, true>(P.part_ptr, P.parts, P.ws_o, P.ws_ml, P.o, P.H, rb + r, h, lane);
+      finish_row<T, D, true>(P.part_ptr, P.parts, P.ws_o, P.o_bytes, P.ws_ml, P.o, P.H, rb + r,
+                             h, lane);
 }
 
 // Matrix-core operand layout used below (16x16 output tiles, 64 lanes;
@@ -749,9 +809,13 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
   }
   // write the segment's partial (O, m, n) for every covered row
   const size_t pbase = static_cast<size_t>(sg.part_base + (rb - sg.row_begin));
-  for (int e = tid; e < nrows * D; e += 256) {
-    const int r = e / D, d = e % D;
-    st_dev(P.ws_o + ((pbase + r) * H + h) * D + d, obuf[r * OS + d]);
+  {
+    const __amdgpu_buffer_rsrc_t rs = part_rsrc(P.ws_o, P.o_bytes);
+    for (int e = tid; e < nrows * (D / 4); e += 256) {
+      const int r = e / (D / 4), d = 4 * (e % (D / 4));
+      const float4 v = *reinterpret_cast<const float4*>(obuf + r * OS + d);
+      st_dev4(rs, part_off(static_cast<int>(pbase) + r, H, D, h, d), v.x, v.y, v.z, v.w);
+    }
   }
   if (w == 0 && g == 0) {
 #pragma unroll
@@ -906,11 +970,12 @@ __device__ __forceinline__ void kcf_f32_block(const KcfParams& P, int seg, int z
     const int r = 16 * t + l16;
     if (r < nrows) {
       const size_t p = static_cast<size_t>(sg.part_base + (rb - sg.row_begin) + r);
-      float* po = P.ws_o + (p * H + h) * D;
+      const __amdgpu_buffer_rsrc_t rs = part_rsrc(P.ws_o, P.o_bytes);
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
         const floatx4 v = acc[dt][t];
-        st_dev4(po + w * (D / 4) + 16 * dt + 4 * g, v[0], v[1], v[2], v[3]);
+        st_dev4(rs, part_off(static_cast<int>(p), H, D, h, w * (D / 4) + 16 * dt + 4 * g), v[0], v[1],
+                v[2], v[3]);
       }
       if (w == 0 && g == 0) {
         float* pml = reinterpret_cast<float*>(P.ws_ml + p * H + h);
@@ -1033,9 +1098,14 @@ hipError_t launch_phases(const TppParams& P, int n_sf, int schedule, int mask, h
                          const SideStream& side) {
   const bool both = (mask & 3) == 3;
   if ((schedule == 1 || schedule == 2) && both) {
-    const int grid = P.n_cf + n_sf;
-    if (grid > 0) tpp_kernel<T, D, NRT><<<grid, 256, 0, s>>>(P);
-    return hipSuccess;
+    // the fused launch always takes 16-row chunk-first blocks
+    if constexpr (NRT == 1) {
+      const int grid = P.n_cf + n_sf;
+      if (grid > 0) tpp_kernel<T, D, NRT><<<grid, 256, 0, s>>>(P);
+      return hipSuccess;
+    } else {
+      return hipErrorInvalidValue;
+    }
   }
   if (schedule == 3 && both && P.n_cf > 0 && n_sf > 0) {
     // chunk-first on the side stream, sequence-first on the caller's stream,
@@ -1067,11 +1137,11 @@ hipError_t launch_all(const AttnArgs& a, const DevWork& w, hipStream_t s, int ma
   TppParams P;
   const bool counting = w.schedule >= 2;  // the last contributor finishes each row
   P.cf = KcfParams{a.q, a.kpool, a.vpool, a.slot_len, w.segs, w.seg_slots, a.ws_o,
-                   reinterpret_cast<float2*>(a.ws_ml), a.H, a.C, a.qscale,
+                   reinterpret_cast<float2*>(a.ws_ml), a.ws_o_bytes, a.H, a.C, a.qscale,
                    counting ? a.cnt : nullptr, a.o, w.part_ptr, w.parts};
   P.sf = KsfParams{a.q, a.o, a.kpool, a.vpool, a.slot_len, w.items, w.priv_slot, w.part_ptr,
-                   w.parts, a.ws_o, reinterpret_cast<float2*>(a.ws_ml), a.H, a.C, a.qscale,
-                   counting ? a.cnt : nullptr};
+                   w.parts, a.ws_o, reinterpret_cast<float2*>(a.ws_ml), a.ws_o_bytes, a.H, a.C,
+                   a.qscale, counting ? a.cnt : nullptr};
   // At most 16 or 32 covered rows per chunk-first block; wider runs take
   // several row blocks, which re-read the chunk. Their block indices differ
   // by a multiple of H, so for H a multiple of 8 they land on the same XCD
@@ -1094,7 +1164,7 @@ hipError_t launch_all(const AttnArgs& a, const DevWork& w, hipStream_t s, int ma
   const bool self_finished = counting && (mask & 3) == 3;
   if ((mask & 4) && w.n_mg > 0 && !self_finished) {
     KmgParams M{a.o, w.mg_rows, w.part_ptr, w.parts, a.ws_o, reinterpret_cast<const float2*>(a.ws_ml),
-                a.H};
+                a.ws_o_bytes, a.H};
     kmg_kernel<T, D><<<dim3(w.n_mg, a.H), 64, 0, s>>>(M);
   }
   return hipGetLastError();

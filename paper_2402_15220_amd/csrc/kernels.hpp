@@ -44,6 +44,7 @@ struct AttnArgs {
   const int32_t* slot_len;
   float* ws_o;   // [n_parts][H][D]
   float* ws_ml;  // [n_parts][H][2] (running max in log2 units, sum)
+  uint32_t ws_o_bytes;  // bytes of the ws_o region (below 4 GiB)
   float qscale;  // softmax scale * log2(e)
   int32_t* cnt;  // [B][H] arrival counters, zero between launches
 };
