@@ -12,8 +12,16 @@ Prints one JSON line: tokens/s (B per call) and µs per call from the timed
 loop, the roofline of the dominant kernel (the fused two-phase kernel,
 HBM-bound) from HIP events on the launch stream, per-phase figures measured
 in isolation, and the CPU oracle timed on the host for the same workload.
-`--cold` additionally times calls after a clean 1 GiB read that evicts the
-caches (kept out of the default run so profiler averages stay comparable).
+Also, unless switched off:
+  cold     calls timed after a clean 1 GiB read that evicts L2 and the
+           256 MB Infinity Cache (the conservative figure: in a model, other
+           layers' K/V pass between two calls of one layer);
+  dynamic  the 64-step decode workload (2048-token prompt, 128 sequences of
+           64..1024 unique tokens, 10% churn every 16 steps): per-step
+           attention time and per-step library time (churn, append, context
+           upload, attention).
+Profiler runs pass --no-cold --no-dynamic so that the per-kernel averages
+cover the bench workload's warm launches only.
 """
 from __future__ import annotations
 
@@ -35,11 +43,13 @@ def _parse():
     ap.add_argument("--config", type=int, default=2, help="workload 2, 3 or 4 (default 2)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle sample time")
-    ap.add_argument("--cold", action="store_true", help="also time calls after a cache-evicting read")
+    ap.add_argument("--no-cold", action="store_true", help="skip the cache-evicted timing")
+    ap.add_argument("--no-dynamic", action="store_true", help="skip the 64-step decode workload")
     ap.add_argument("--seg", type=int, default=0, help="chunk-first segment size (0: library default)")
     ap.add_argument("--split", type=int, default=-1, help="sequence-first split (-1: library default)")
     ap.add_argument("--schedule", type=int, default=-1,
-                    help="0 sequential, 1 fused launch, 2 concurrent streams (-1: library default)")
+                    help="0 sequential, 1 fused + merge launch, 2 fused with in-kernel merge, "
+                         "3 two streams (-1: library default)")
     return ap.parse_args()
 
 
@@ -164,12 +174,16 @@ def main():
                               "mfma_util": kcf_tflops / PEAK_MFMA_TFLOPS["f16"],
                               "GBps": (model["shared_kv"] + model["q"]) / (kcf_us * 1e-6) / 1e9},
     }
-    if args.cold:
+    if not args.no_cold:
         out["cold"] = cold_times(call, cache, model)
+    cache.close()
+    del cache, q, o
+    torch.cuda.empty_cache()
+    if not args.no_dynamic:
+        out["dynamic"] = dynamic_run()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, rows, args.cpu_seconds)
     print(json.dumps(out), flush=True)
-    cache.close()
 
 
 def counter_traffic(workload):
@@ -211,8 +225,94 @@ def cold_times(call, cache, model, n=30):
         evs.append((a, b))
     torch.cuda.synchronize()
     us = float(np.median([a.elapsed_time(b) * 1e3 for a, b in evs]))
-    return {"us_per_call": us, "tok_per_s": model["B"] / (us * 1e-6),
-            "GBps": model["total"] / (us * 1e-6) / 1e9}
+    from paper_2402_15220_amd.roofline import PEAK_HBM_GBPS
+
+    gbps = model["total"] / (us * 1e-6) / 1e9
+    return {"us_per_call": us, "tok_per_s": model["B"] / (us * 1e-6), "GBps": gbps,
+            "frac": gbps / PEAK_HBM_GBPS, "calls": n,
+            "flush": "clean 1 GiB read between calls; median of per-call event pairs "
+                     "(each pair adds ~2 us of marker overhead)"}
+
+
+def dynamic_run():
+    """The 64-step decode workload: every step appends one token to each live
+    sequence (after churn on steps 16, 32, 48), then attends. Inputs of all
+    steps are generated and copied to the GPU first; each step then times the
+    library calls only: attention alone with events, and the whole step
+    (remove/insert, append, row order, q permutation, attention) on the host
+    clock up to a synchronisation."""
+    import numpy as np
+    import torch
+
+    from paper_2402_15220_amd.cache import Cache
+    from workloads import make_dynamic
+
+    t_gen = time.perf_counter()
+    wl = make_dynamic()
+    steps = list(wl.steps())
+    nodes = sum(-(-len(s) // wl.c) for s in wl.segments) + len(steps) * 128 // wl.c + 256
+    cache = Cache(wl.c, wl.H, wl.d, nodes, dtype=torch.float16)
+    seg_dev = {}
+
+    def dev_seg(i):
+        if i not in seg_dev:
+            seg_dev[i] = (torch.from_numpy(wl.segments[i].k).cuda(), torch.from_numpy(wl.segments[i].v).cuda())
+        return seg_dev[i]
+
+    def full_kv(s):
+        return (torch.cat([dev_seg(i)[0] for i in s.segs]), torch.cat([dev_seg(i)[1] for i in s.segs]))
+
+    for s in wl.seqs:
+        k, v = full_kv(s)
+        cache.insert(s.seq_id, s.tokens(wl.segments), k, v)
+        del k, v
+    dev_steps = []
+    for st in steps:
+        added = []
+        if st.churn:
+            for s in st.churn.added:
+                k, v = full_kv(s)
+                added.append((s.seq_id, s.tokens(wl.segments), k, v))
+        dev_steps.append((st, added, torch.from_numpy(st.k).cuda(), torch.from_numpy(st.v).cuda(),
+                          torch.from_numpy(st.q).cuda()))
+    q_rows = torch.empty((256, wl.H, wl.d), dtype=torch.float16, device="cuda")
+    o = torch.empty_like(q_rows)
+    torch.cuda.synchronize()
+    t_gen = time.perf_counter() - t_gen
+    up0 = cache.stats()["uploads"]
+
+    att_us, step_us, rows = [], [], []
+    for st, added, k, v, q in dev_steps:
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        t0 = time.perf_counter()
+        if st.churn:
+            for sid in st.churn.removed:
+                cache.remove(sid)
+            for sid, toks, kk, vv in added:
+                cache.insert(sid, toks, kk, vv)
+        cache.append(st.live, st.tokens, k, v)
+        order = cache.seq_order()
+        pos = np.searchsorted(st.live, order)
+        n = len(order)
+        idx = torch.from_numpy(pos).cuda(non_blocking=True)
+        torch.index_select(q, 0, idx, out=q_rows[:n])
+        a.record()
+        cache.attention(q_rows[:n], out=o[:n])
+        b.record()
+        b.synchronize()
+        step_us.append((time.perf_counter() - t0) * 1e6)
+        att_us.append(a.elapsed_time(b) * 1e3)
+        rows.append(n)
+    up = cache.stats()["uploads"] - up0
+    cache.close()
+    del cache, seg_dev, dev_steps
+    torch.cuda.empty_cache()
+    return {"workload": wl.name, "steps": len(att_us), "rows_per_step": int(np.median(rows)),
+            "attention_us_mean": float(np.mean(att_us)), "attention_us_median": float(np.median(att_us)),
+            "step_us_mean": float(np.mean(step_us)), "step_us_median": float(np.median(step_us)),
+            "tok_per_s": float(sum(rows) / (sum(att_us) * 1e-6)),
+            "context_uploads": int(up), "setup_s": t_gen}
 
 
 def cpu_baseline(wl, rows, seconds):
