@@ -1,0 +1,214 @@
+"""The paper's microkernel experiments, re-run on one MI355X with synthetic data.
+
+    python -m paper_2402_15220_amd.sweeps [table3] [fig3] [fig4]
+
+Workload of the experiments section (microkernel evaluation): batch mode, b
+sequences whose n_p prompt tokens start with n_s shared tokens, h=32 heads,
+d=128, chunk c=64, fp16.
+
+  table3  one decode call over the prompts (Table 3 grid: n_p in 1024, 2048,
+          4096 and n_s in 0, n_p/2, 3n_p/4, n_p; b=32). Reported warm
+          (back-to-back calls) and cold (after a clean 1 GiB read that evicts
+          L2 and the Infinity Cache).
+  fig3    decode from an n_s-token shared prompt, one appended token per
+          sequence per step, up to n_c completion tokens (b=32); token rate
+          n_c*b/t at the checkpoints of the Figure 3 table, with t the summed
+          attention time of the steps (the paper's kernel-only measure), and
+          the rate of the whole library step (append, context upload,
+          attention) on the host clock.
+  fig4    the same decode for n_c=64 tokens, n_s in 1024 and 2048, b from 16
+          to 96 (Figure 4's batch sweep).
+
+Token ids follow the seeded recipe of ``workloads`` (uniform ids, distinct
+first unique tokens); K, V and q are N(0,1) fp16 draws of a seeded torch
+generator on the GPU (timing does not depend on the values, and building
+gigabytes of host arrays would dominate the run). The paper's A100 numbers
+(Table 3 and the Figure 3 table) ride along for context only.
+
+Each result is one JSON line on stdout.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+from .cache import Cache
+from .roofline import PEAK_HBM_GBPS, call_model
+
+H, D, C = 32, 128, 64
+
+# ChunkAttn latency on A100 (Table 3), µs, keyed by (n_p, n_s), b=32
+PAPER_TABLE3_US = {
+    (1024, 0): 332.50, (1024, 512): 198.87, (1024, 768): 131.21, (1024, 1024): 56.00,
+    (2048, 0): 655.44, (2048, 1024): 384.37, (2048, 1536): 247.14, (2048, 2048): 110.48,
+    (4096, 0): 1301.78, (4096, 2048): 747.56, (4096, 3072): 477.66, (4096, 4096): 206.22,
+}
+# ChunkAttn token rate on A100 (Figure 3 table), tokens/s, keyed by (n_s, n_c), b=32
+PAPER_FIG3_TPS = {
+    (1024, 256): 241.93e3, (1024, 512): 186.44e3, (1024, 1024): 127.85e3,
+    (2048, 512): 145.41e3, (2048, 1024): 107.37e3, (2048, 2048): 70.33e3,
+    (4096, 512): 101.69e3, (4096, 1024): 81.69e3, (4096, 2048): 58.33e3, (4096, 4096): 37.05e3,
+}
+
+
+def _root():
+    return os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def build_batch(b, n_p, n_s, seed, spare_slots=0):
+    """Insert b prompts of n_p tokens sharing their first n_s; returns the cache."""
+    sys.path.insert(0, _root())
+    from workloads import sweep_tokens
+
+    shared, uniq = sweep_tokens(b, n_p, n_s, seed)
+    slots = -(-n_s // C) + b * (-(-(n_p - n_s) // C)) + spare_slots + 1
+    cache = Cache(C, H, D, slots, dtype=torch.float16)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    ks = torch.randn((n_s, H, D), generator=g, device="cuda", dtype=torch.float16)
+    vs = torch.randn((n_s, H, D), generator=g, device="cuda", dtype=torch.float16)
+    for i in range(b):
+        n_u = n_p - n_s
+        ku = torch.randn((n_u, H, D), generator=g, device="cuda", dtype=torch.float16)
+        vu = torch.randn((n_u, H, D), generator=g, device="cuda", dtype=torch.float16)
+        toks = np.concatenate([shared, uniq[i]]).astype(np.int32)
+        cache.insert(i, toks, torch.cat([ks, ku]), torch.cat([vs, vu]))
+    torch.cuda.synchronize()
+    return cache, g
+
+
+def _events_mean(fn, n):
+    fn()
+    torch.cuda.synchronize()
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(n):
+        fn()
+    b.record()
+    b.synchronize()
+    return a.elapsed_time(b) * 1e3 / n
+
+
+def _cold_median(fn, flush, n):
+    evs = []
+    for _ in range(n):
+        flush.sum()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        fn()
+        b.record()
+        evs.append((a, b))
+    torch.cuda.synchronize()
+    return float(np.median([a.elapsed_time(b) * 1e3 for a, b in evs]))
+
+
+def table3(flush, b=32, warm_calls=100, cold_calls=20):
+    for n_p in (1024, 2048, 4096):
+        for n_s in (0, n_p // 2, 3 * n_p // 4, n_p):
+            cache, g = build_batch(b, n_p, n_s, seed=7000 + n_p + n_s)
+            q = torch.randn((b, H, D), generator=g, device="cuda", dtype=torch.float16)
+            o = torch.empty_like(q)
+            model = call_model(cache.tables(), H, D, 2)
+
+            def call():
+                cache.attention(q, out=o)
+
+            warm = _events_mean(call, warm_calls)
+            cold = _cold_median(call, flush, cold_calls)
+            paper = PAPER_TABLE3_US[(n_p, n_s)]
+            print(json.dumps({
+                "sweep": "table3", "b": b, "n_p": n_p, "n_s": n_s,
+                "us_warm": round(warm, 2), "us_cold": round(cold, 2),
+                "tok_per_s_cold": round(b / (cold * 1e-6)),
+                "algorithmic_bytes": model["total"],
+                "hbm_frac_warm": round(model["total"] / (warm * 1e-6) / 1e9 / PEAK_HBM_GBPS, 4),
+                "hbm_frac_cold": round(model["total"] / (cold * 1e-6) / 1e9 / PEAK_HBM_GBPS, 4),
+                "seg_chunks": cache.stats()["seg_chunks"],
+                "paper_a100_us": paper, "a100_over_mi355x_cold": round(paper / cold, 2),
+            }), flush=True)
+            cache.close()
+            del cache, q, o
+            torch.cuda.empty_cache()
+
+
+def decode_run(b, n_s, n_c, checkpoints, seed):
+    """Decode n_c steps from b copies of an n_s-token shared prompt (the
+    first completion token makes the sequences diverge); returns the token
+    rates at the checkpoints."""
+    sys.path.insert(0, _root())
+    from workloads import decode_tokens
+
+    cache, g = build_batch(b, n_s, n_s, seed, spare_slots=b * (-(-n_c // C) + 1))
+    toks = decode_tokens(b, n_c, seed + 1)
+    ids = np.arange(b, dtype=np.int64)
+    o = torch.empty((b, H, D), dtype=torch.float16, device="cuda")
+    att_us, step_us = [], []
+    for step in range(n_c):
+        k = torch.randn((b, H, D), generator=g, device="cuda", dtype=torch.float16)
+        v = torch.randn((b, H, D), generator=g, device="cuda", dtype=torch.float16)
+        q = torch.randn((b, H, D), generator=g, device="cuda", dtype=torch.float16)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        cache.append(ids, toks[step], k, v)
+        a = torch.cuda.Event(enable_timing=True)
+        e = torch.cuda.Event(enable_timing=True)
+        a.record()
+        cache.attention(q, out=o)
+        e.record()
+        e.synchronize()
+        step_us.append((time.perf_counter() - t0) * 1e6)
+        att_us.append(a.elapsed_time(e) * 1e3)
+    cache.close()
+    torch.cuda.empty_cache()
+    out = []
+    for n in checkpoints:
+        t_att = sum(att_us[:n]) * 1e-6
+        t_step = sum(step_us[:n]) * 1e-6
+        out.append((n, n * b / t_att, n * b / t_step, float(np.mean(att_us[:n]))))
+    return out
+
+
+def fig3(b=32):
+    for n_s, n_cs in ((1024, (256, 512, 1024)), (2048, (512, 1024, 2048)),
+                      (4096, (512, 1024, 2048, 4096))):
+        for n_c, tps, tps_step, mean_us in decode_run(b, n_s, max(n_cs), n_cs, seed=8000 + n_s):
+            paper = PAPER_FIG3_TPS[(n_s, n_c)]
+            print(json.dumps({
+                "sweep": "fig3", "b": b, "n_s": n_s, "n_c": n_c,
+                "tok_per_s_attention": round(tps), "tok_per_s_library_step": round(tps_step),
+                "attention_us_mean": round(mean_us, 2),
+                "paper_a100_tok_per_s": paper, "mi355x_over_a100": round(tps / paper, 2),
+            }), flush=True)
+
+
+def fig4(n_c=64):
+    for n_s in (1024, 2048):
+        for b in (16, 32, 48, 64, 80, 96):
+            (_, tps, tps_step, mean_us), = decode_run(b, n_s, n_c, (n_c,), seed=9000 + n_s + b)
+            print(json.dumps({
+                "sweep": "fig4", "b": b, "n_s": n_s, "n_c": n_c,
+                "tok_per_s_attention": round(tps), "tok_per_s_library_step": round(tps_step),
+                "attention_us_mean": round(mean_us, 2),
+            }), flush=True)
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("which", nargs="*", default=["table3", "fig3", "fig4"])
+    args = ap.parse_args(argv)
+    torch.cuda.set_device(0)
+    flush = torch.ones(1 << 29, dtype=torch.float16, device="cuda")  # 1 GiB
+    for w in args.which:
+        {"table3": lambda: table3(flush), "fig3": fig3, "fig4": fig4}[w]()
+
+
+if __name__ == "__main__":
+    main()

@@ -17,4 +17,6 @@ from .synth import (  # noqa: F401
     make_dynamic,
     random_op_script,
     prefix_keyed_kv,
+    sweep_tokens,
+    decode_tokens,
 )

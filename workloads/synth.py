@@ -284,6 +284,31 @@ def make_dynamic(config: int = 5, n_steps: int = 64, B: int = 128,
                            segments, seqs, n_steps, churn_steps, int(round(0.1 * B)), rng, redraws)
 
 
+def sweep_tokens(b: int, n_p: int, n_s: int, seed: int):
+    """Token ids of a batch of b prompts of n_p tokens whose first n_s tokens
+    are one shared prefix (the paper's microkernel workload). The first
+    unique token of each prompt is redrawn until it differs from the other
+    prompts' (so the shared part is exactly n_s tokens); with n_s = n_p all
+    prompts are the same. Returns (shared [n_s], list of b unique arrays)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    shared = rng.integers(0, VOCAB, size=n_s).astype(np.int32)
+    firsts, uniq = set(), []
+    for _ in range(b):
+        if n_p > n_s:
+            t, _ = _draw_tokens(rng, n_p - n_s, firsts)
+            firsts.add(int(t[0]))
+        else:
+            t = np.zeros(0, np.int32)
+        uniq.append(t)
+    return shared, uniq
+
+
+def decode_tokens(b: int, n_c: int, seed: int) -> np.ndarray:
+    """Completion token ids [n_c, b] for a decode run (one per sequence per step)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    return rng.integers(0, VOCAB, size=(n_c, b)).astype(np.int32)
+
+
 # ---------------------------------------------------------------------------
 # Random operation scripts for tree tests (small alphabets force sharing,
 # splits, sibling collisions and prefix sequences).
