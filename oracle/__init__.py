@@ -17,7 +17,9 @@ It is a plain, slow, obviously-correct restatement of ChunkAttention
                  sequence and head, softmax(scale * K q) V over the K/V rows on
                  the sequence's root-to-leaf path, in float64; and, as a
                  self-check only, the same result assembled chunk by chunk with
-                 partial_attn (Eqn 1) and attn_reduce (Eqn 2).
+                 partial_attn (Eqn 1) and attn_reduce (Eqn 2); plus causal
+                 prefill attention for a sequence's last tokens over its
+                 whole path (Section 3.2, prefill paragraph).
 """
 from .tree import OracleTree, PoolExhausted  # noqa: F401
 from .tables import tables, Tables  # noqa: F401
@@ -28,4 +30,5 @@ from .attention import (  # noqa: F401
     partial_attn,
     attn_reduce,
     path_kv,
+    prefill_attention,
 )

@@ -56,6 +56,31 @@ def dense_attention(tree, row_seq, q, scale):
     return dense_attention_rows(tree, row_seq, q, scale)
 
 
+def prefill_attention(tree, sid, q, scale, heads=None, queries=None):
+    """Causal attention for the last n_q tokens of sequence ``sid`` over its
+    whole K/V (Section 3.2, prefill paragraph: after the prefix lookup the
+    suffix's K/V joins the tree and ordinary self-attention runs over the
+    entire K/V of the sequence).
+
+    q: [n_q, H, d], query i belongs to position p = L - n_q + i and attends
+    to positions 0..p of the root-to-leaf K/V. Returns float64
+    [len(queries), len(heads), d].
+    """
+    k, v = path_kv(tree, sid)
+    L = k.shape[0]
+    n_q, H, d = q.shape
+    if n_q > L:
+        raise ValueError("more queries than tokens")
+    heads = np.arange(H) if heads is None else np.asarray(heads)
+    queries = range(n_q) if queries is None else queries
+    out = np.empty((len(queries), len(heads), d), np.float64)
+    for j, i in enumerate(queries):
+        p = L - n_q + i
+        out[j] = _softmax_attend(q[i, heads].astype(np.float64), k[: p + 1, heads],
+                                 v[: p + 1, heads], scale)
+    return out
+
+
 # -- Eqn 1 / Eqn 2, for the structural self-check only ----------------------
 
 def partial_attn(Q, K, V, scale):

@@ -12,7 +12,7 @@ import pytest
 import torch
 
 from oracle import (OracleTree, PoolExhausted, dense_attention, dense_attention_rows,
-                    path_kv, structured_attention, tables)
+                    path_kv, prefill_attention, structured_attention, tables)
 from workloads import make_dynamic, make_static, prefix_keyed_kv, random_op_script
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
@@ -430,3 +430,99 @@ def test_plant_eqn2_swap_is_caught(monkeypatch):
     monkeypatch.setattr(A, "attn_reduce", bad_reduce)
     bad = A.structured_attention(t, tb.row_seq, q, wl.scale)
     assert np.abs(bad - good).max() > 1e-3
+
+
+# -- prefill with prefix reuse (Section 3.2, prefill paragraph) --------------
+
+def _prefill_case(c, n_shared=40, n_new=23, H=2, d=16, seed=3):
+    """A tree where a second sequence reuses the first one's prefix."""
+    rng = np.random.default_rng(seed)
+    shared = rng.integers(0, 100, n_shared).astype(np.int32)
+    a = np.concatenate([shared, rng.integers(100, 200, 9).astype(np.int32)])
+    b = np.concatenate([shared, rng.integers(200, 300, n_new).astype(np.int32)])
+    t = OracleTree(c=c, with_kv=True)
+    ka, va = prefix_keyed_kv(seed, a, 0, H, d, np.float64)
+    kb, vb = prefix_keyed_kv(seed, b, 0, H, d, np.float64)
+    t.insert(0, a, ka, va)
+    t.insert(1, b, kb, vb)
+    q = rng.standard_normal((n_new, H, d))
+    return t, b, kb, vb, q
+
+
+def _sdpa_masked(q, k, v, mask, scale):
+    """torch SDPA in float64: q [n, H, d], k/v [L, H, d], mask [n, L] (True = attend)."""
+    qq = torch.from_numpy(q.transpose(1, 0, 2).copy())
+    kk = torch.from_numpy(k.transpose(1, 0, 2).copy())
+    vv = torch.from_numpy(v.transpose(1, 0, 2).copy())
+    o = torch.nn.functional.scaled_dot_product_attention(qq, kk, vv, attn_mask=torch.from_numpy(mask),
+                                                         scale=scale)
+    return o.numpy().transpose(1, 0, 2)
+
+
+def test_prefill_matches_masked_library_attention():
+    """Suffix queries over prefix + suffix: torch SDPA with a position mask."""
+    for c in (1, 4, 7, 64):
+        t, toks, k, v, q = _prefill_case(c)
+        L, n = len(toks), q.shape[0]
+        mask = np.arange(L)[None, :] <= (L - n + np.arange(n))[:, None]
+        ref = _sdpa_masked(q, k, v, mask, 0.25)
+        o = prefill_attention(t, 1, q, 0.25)
+        np.testing.assert_allclose(o, ref, rtol=0, atol=1e-12)
+
+
+def test_prefill_whole_prompt_is_causal_attention():
+    """n_q = L (nothing matched): SDPA's own causal mode."""
+    rng = np.random.default_rng(5)
+    toks = rng.integers(0, 50, 37).astype(np.int32)
+    k, v = prefix_keyed_kv(5, toks, 0, 3, 8, np.float64)
+    t = OracleTree(c=5, with_kv=True)
+    t.insert(0, toks, k, v)
+    q = rng.standard_normal((37, 3, 8))
+    qq = torch.from_numpy(q.transpose(1, 0, 2).copy())
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        qq, torch.from_numpy(k.transpose(1, 0, 2).copy()), torch.from_numpy(v.transpose(1, 0, 2).copy()),
+        is_causal=True).numpy().transpose(1, 0, 2)
+    np.testing.assert_allclose(prefill_attention(t, 0, q, 1 / np.sqrt(8)), ref, rtol=0, atol=1e-12)
+
+
+def test_prefill_last_query_is_decode_attention():
+    """The last query sees the whole sequence: the decode result of that row."""
+    t, toks, k, v, q = _prefill_case(4)
+    tb = tables(t)
+    r = int(np.nonzero(tb.row_seq == 1)[0][0])
+    qrows = np.zeros((len(tb.row_seq),) + q.shape[1:])
+    qrows[r] = q[-1]
+    dec = dense_attention_rows(t, tb.row_seq, qrows, 0.3, rows=[r])
+    pre = prefill_attention(t, 1, q, 0.3, queries=[q.shape[0] - 1])
+    np.testing.assert_allclose(pre, dec, rtol=0, atol=1e-13)
+
+
+def test_prefill_first_token_query_sees_only_itself():
+    """Query at position 0 (n_q = L) attends to one token: o = v_0 exactly."""
+    t, toks, k, v, q = _prefill_case(4)
+    L = len(toks)
+    qq = np.random.default_rng(1).standard_normal((L, 2, 16))
+    o = prefill_attention(t, 1, qq, 0.5, queries=[0])
+    np.testing.assert_allclose(o[0], v[0], rtol=0, atol=1e-15)
+
+
+def test_plant_off_by_one_causal_mask_is_caught(monkeypatch):
+    """A mask that also shows the next token must fail the SDPA pin."""
+    import oracle.attention as A
+
+    real = A._softmax_attend
+    t, toks, k, v, q = _prefill_case(4)
+    L, n = len(toks), q.shape[0]
+
+    def leaky(qv, kk, vv, scale):
+        # one extra row beyond the causal limit whenever one exists
+        m = kk.shape[0]
+        if m < L:
+            kk, vv = k[: m + 1], v[: m + 1]
+        return real(qv, kk, vv, scale)
+
+    monkeypatch.setattr(A, "_softmax_attend", leaky)
+    mask = np.arange(L)[None, :] <= (L - n + np.arange(n))[:, None]
+    ref = _sdpa_masked(q, k, v, mask, 0.25)
+    o = A.prefill_attention(t, 1, q, 0.25)
+    assert np.abs(o - ref).max() > 1e-3
