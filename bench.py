@@ -20,8 +20,11 @@ Also, unless switched off:
            64..1024 unique tokens, 10% churn every 16 steps): per-step
            attention time and per-step library time (churn, append, context
            upload, attention).
-Profiler runs pass --no-cold --no-dynamic so that the per-kernel averages
-cover the bench workload's warm launches only.
+  prefill  a 33rd sequence joins the bench tree with the shared prompt plus
+           512 new tokens; causal attention of the new tokens over all 1536
+           positions (prefill with prefix reuse), against the MFMA peak.
+Profiler runs pass --no-cold --no-dynamic --no-prefill so that the
+per-kernel averages cover the bench workload's warm launches only.
 """
 from __future__ import annotations
 
@@ -45,6 +48,7 @@ def _parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle sample time")
     ap.add_argument("--no-cold", action="store_true", help="skip the cache-evicted timing")
     ap.add_argument("--no-dynamic", action="store_true", help="skip the 64-step decode workload")
+    ap.add_argument("--no-prefill", action="store_true", help="skip the prefill-with-prefix-reuse timing")
     ap.add_argument("--seg", type=int, default=0, help="chunk-first segment size (0: library default)")
     ap.add_argument("--split", type=int, default=-1, help="sequence-first split (-1: library default)")
     ap.add_argument("--schedule", type=int, default=-1,
@@ -181,6 +185,8 @@ def main():
     torch.cuda.empty_cache()
     if not args.no_dynamic:
         out["dynamic"] = dynamic_run()
+    if not args.no_prefill:
+        out["prefill"] = prefill_run()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, rows, args.cpu_seconds)
     print(json.dumps(out), flush=True)
@@ -232,6 +238,59 @@ def cold_times(call, cache, model, n=30):
             "frac": gbps / PEAK_HBM_GBPS, "calls": n,
             "flush": "clean 1 GiB read between calls; median of per-call event pairs "
                      "(each pair adds ~2 us of marker overhead)"}
+
+
+def prefill_run(n=100):
+    """Prefill with prefix reuse: the joining sequence's 512 new tokens attend
+    causally over its 1536 positions (1024 reused from the tree). Event-timed
+    back-to-back calls on the launch stream."""
+    import numpy as np
+    import torch
+
+    from paper_2402_15220_amd.cache import Cache
+    from paper_2402_15220_amd.roofline import PEAK_MFMA_TFLOPS
+    from workloads import make_prefill_join
+
+    pj = make_prefill_join()
+    wl = pj.static
+    cache = Cache(wl.c, wl.H, wl.d, 400, dtype=torch.float16)
+    seg_dev = [(torch.from_numpy(s.k).cuda(), torch.from_numpy(s.v).cuda()) for s in wl.segments]
+    matched = 0
+    for s in wl.seqs + [pj.seq]:
+        matched = cache.insert(s.seq_id, s.tokens(wl.segments), torch.cat([seg_dev[i][0] for i in s.segs]),
+                               torch.cat([seg_dev[i][1] for i in s.segs]))
+    q = torch.from_numpy(pj.q).cuda()
+    o = torch.empty_like(q)
+    sid = pj.seq.seq_id
+
+    def call():
+        cache.prefill(sid, q, out=o)
+
+    call()
+    torch.cuda.synchronize()
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(n):
+        call()
+    b.record()
+    b.synchronize()
+    us = a.elapsed_time(b) * 1e3 / n
+    L = len(pj.seq.tokens(wl.segments))
+    n_q = pj.n_new
+    ctx = sum(L - n_q + i + 1 for i in range(n_q))      # attended positions over all queries
+    flops = 4 * wl.H * wl.d * ctx
+    kv_bytes = 2 * L * wl.H * wl.d * 2
+    tflops = flops / (us * 1e-6) / 1e12
+    cache.close()
+    del cache, seg_dev
+    torch.cuda.empty_cache()
+    return {"workload": f"join_{wl.name}_plus_{n_q}_new_tokens", "n_q": n_q, "context": L,
+            "matched": int(matched), "kernel": "kpf_kernel", "us_per_call": us,
+            "tok_per_s": n_q / (us * 1e-6), "flops": flops, "tflops": tflops,
+            "roofline": {"bound": "mfma", "achieved": tflops, "peak": PEAK_MFMA_TFLOPS["f16"],
+                         "unit": "TFLOP/s", "frac": tflops / PEAK_MFMA_TFLOPS["f16"]},
+            "kv_bytes": kv_bytes}
 
 
 def dynamic_run():

@@ -185,6 +185,23 @@ ca_status ca_workspace_size(const ca_cache* cache, size_t* bytes);
 ca_status ca_attention(ca_cache* cache, const void* q, void* o, float scale, void* ws,
                        size_t ws_bytes, void* stream);
 
+/* Prefill attention with prefix reuse (Section 3.2, prefill paragraph): a
+ * joining sequence's matched prefix keeps its K/V in the tree, its unmatched
+ * suffix is written by ca_insert/ca_extend, and attention then runs over the
+ * sequence's entire K/V. This computes it for the sequence's last n_q
+ * tokens: query i (position L - n_q + i, L = the sequence's length) attends
+ * causally to positions 0 .. L - n_q + i of its root-to-leaf chunks.
+ *   q      device [n_q][H][d], 16-byte aligned; o the same shape, written
+ *   n_q    0 <= n_q <= L (0 is a no-op); typically L - matched
+ *   scale  softmax scale applied to q.k; 0 means 1/sqrt(d)
+ * fp16 caches only. Enqueue on the stream of the insert/extend that wrote
+ * the K/V rows. The path (chunk slots and start positions, 8 bytes per
+ * chunk) is copied to the device through library-owned pinned staging.
+ * Errors: INVALID (table-only or fp32 cache, null or misaligned q/o,
+ * n_q > L), NOT_FOUND, DEVICE. */
+ca_status ca_prefill_attention(ca_cache* cache, int64_t seq_id, const void* q, void* o,
+                               int64_t n_q, float scale, void* stream);
+
 /* Host views of the canonical tables for the current tree (see ca_tables).
  * Lengths reflect every call made so far. */
 ca_status ca_export_tables(const ca_cache* cache, ca_tables* out);

@@ -108,6 +108,20 @@ class Cache:
                        self.stream())
         return out
 
+    def prefill(self, seq_id, q, out=None, scale: float = 0.0):
+        """Causal attention of sequence ``seq_id``'s last q.shape[0] tokens over
+        its whole K/V (prefill after a prefix-matched insert). q: [n_q, H, d]."""
+        if self.table_only:
+            raise ValueError("table-only cache has no attention")
+        if q.dtype != self.dtype or q.dim() != 3 or tuple(q.shape[1:]) != (self.H, self.d) \
+                or not q.is_contiguous() or not q.is_cuda:
+            raise ValueError(f"q must be contiguous {self.dtype} [n_q,{self.H},{self.d}] on the GPU")
+        if out is None:
+            out = torch.empty_like(q)
+        B.ca_prefill_attention(self.h, seq_id, q.data_ptr(), out.data_ptr(), q.shape[0], scale,
+                               self.stream())
+        return out
+
     def close(self):
         if self.h is not None:
             B.ca_destroy(self.h)

@@ -52,6 +52,74 @@ int env_int(const char* name, int dflt) {
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
+// Double-buffered pinned host staging for small host-to-device copies on a
+// stream: a buffer is written again only after the copy that last read it
+// has completed.
+struct PinnedStaging {
+  char* h[2] = {nullptr, nullptr};
+  size_t cap[2] = {0, 0};
+  hipEvent_t ev[2] = {nullptr, nullptr};
+  bool used[2] = {false, false};
+  int next = 0;
+
+  PinnedStaging() = default;
+  PinnedStaging(const PinnedStaging&) = delete;
+  PinnedStaging& operator=(const PinnedStaging&) = delete;
+  ~PinnedStaging() {
+    for (int i = 0; i < 2; ++i) {
+      if (h[i]) (void)hipHostFree(h[i]);
+      if (ev[i]) (void)hipEventDestroy(ev[i]);
+    }
+  }
+  // A host buffer of at least `bytes` for the next copy.
+  ca_status acquire(size_t bytes, char** out) {
+    const int i = next;
+    hipError_t e;
+    if (!ev[i] && (e = hipEventCreateWithFlags(&ev[i], hipEventDisableTiming)) != hipSuccess)
+      return hip_fail(e, "staging event");
+    if (used[i] && (e = hipEventSynchronize(ev[i])) != hipSuccess) return hip_fail(e, "staging wait");
+    if (bytes > cap[i]) {
+      if (h[i]) (void)hipHostFree(h[i]);
+      h[i] = nullptr;
+      cap[i] = 0;
+      const size_t c = align_up(std::max<size_t>(bytes * 2, 4096), 4096);
+      if ((e = hipHostMalloc(reinterpret_cast<void**>(&h[i]), c, hipHostMallocDefault)) != hipSuccess)
+        return hip_fail(e, "staging alloc");
+      cap[i] = c;
+    }
+    *out = h[i];
+    return CA_OK;
+  }
+  // Copy the acquired buffer's first `bytes` to `dst` on `stream`.
+  ca_status copy(void* dst, size_t bytes, hipStream_t stream) {
+    const int i = next;
+    hipError_t e;
+    if ((e = hipMemcpyAsync(dst, h[i], bytes, hipMemcpyHostToDevice, stream)) != hipSuccess)
+      return hip_fail(e, "staging copy");
+    if ((e = hipEventRecord(ev[i], stream)) != hipSuccess) return hip_fail(e, "staging record");
+    used[i] = true;
+    next ^= 1;
+    return CA_OK;
+  }
+};
+
+// Grow-only device buffer; the old one is freed after the stream drains
+// (kernels already enqueued may still read it).
+ca_status ensure_device(char** p, size_t* cap, size_t need, hipStream_t stream, const char* what) {
+  if (need <= *cap) return CA_OK;
+  hipError_t e;
+  if (*p) {
+    if ((e = hipStreamSynchronize(stream)) != hipSuccess) return hip_fail(e, what);
+    (void)hipFree(*p);
+    *p = nullptr;
+    *cap = 0;
+  }
+  const size_t c = align_up(std::max<size_t>(need * 2, 4096), 4096);
+  if ((e = hipMalloc(reinterpret_cast<void**>(p), c)) != hipSuccess) return hip_fail(e, what);
+  *cap = c;
+  return CA_OK;
+}
+
 }  // namespace
 
 struct ca_cache {
@@ -74,11 +142,10 @@ struct ca_cache {
   size_t d_blob_cap = 0;
   int32_t* d_cnt = nullptr;  // [B][H] arrival counters of the partial-writing schedules
   size_t d_cnt_cap = 0;
-  char* h_stage[2] = {nullptr, nullptr};
-  size_t h_stage_cap[2] = {0, 0};
-  hipEvent_t ev[2] = {nullptr, nullptr};
-  bool ev_used[2] = {false, false};
-  int stage = 0;
+  PinnedStaging work_stage;     // kernel context uploads
+  PinnedStaging prefill_stage;  // prefill paths
+  char* d_path = nullptr;       // prefill path on the device
+  size_t d_path_cap = 0;
   ca::DevWork dw;
   bool dw_valid = false;
   int64_t uploads = 0;
@@ -94,10 +161,7 @@ struct ca_cache {
     if (side.fork) (void)hipEventDestroy(side.fork);
     if (side.join) (void)hipEventDestroy(side.join);
     if (side.stream) (void)hipStreamDestroy(side.stream);
-    for (int i = 0; i < 2; ++i) {
-      if (h_stage[i]) (void)hipHostFree(h_stage[i]);
-      if (ev[i]) (void)hipEventDestroy(ev[i]);
-    }
+    if (d_path) (void)hipFree(d_path);
   }
 
   size_t esize() const { return cfg.dtype == CA_FP16 ? 2 : 4; }
@@ -137,41 +201,10 @@ struct ca_cache {
     const size_t o_mg = place(W.mg_rows.size() * 4);
     const size_t total = std::max<size_t>(off, 16);
 
-    hipError_t e;
-    if (total > d_blob_cap) {
-      if (d_blob) {
-        // kernels already enqueued may still read the old blob
-        if ((e = hipStreamSynchronize(stream)) != hipSuccess) return hip_fail(e, "upload sync");
-        (void)hipFree(d_blob);
-        d_blob = nullptr;
-        d_blob_cap = 0;
-      }
-      const size_t cap = align_up(std::max<size_t>(total * 2, 4096), 4096);
-      if ((e = hipMalloc(reinterpret_cast<void**>(&d_blob), cap)) != hipSuccess)
-        return hip_fail(e, "upload alloc");
-      d_blob_cap = cap;
-    }
-    const int i = stage;
-    stage ^= 1;
-    if (!ev[i]) {
-      if ((e = hipEventCreateWithFlags(&ev[i], hipEventDisableTiming)) != hipSuccess)
-        return hip_fail(e, "upload event");
-    }
-    if (ev_used[i]) {
-      if ((e = hipEventSynchronize(ev[i])) != hipSuccess) return hip_fail(e, "upload wait");
-    }
-    if (total > h_stage_cap[i]) {
-      if (h_stage[i]) (void)hipHostFree(h_stage[i]);
-      h_stage[i] = nullptr;
-      const size_t cap = align_up(std::max<size_t>(total * 2, 4096), 4096);
-      if ((e = hipHostMalloc(reinterpret_cast<void**>(&h_stage[i]), cap, hipHostMallocDefault)) !=
-          hipSuccess) {
-        h_stage_cap[i] = 0;
-        return hip_fail(e, "upload staging");
-      }
-      h_stage_cap[i] = cap;
-    }
-    char* h = h_stage[i];
+    ca_status st = ensure_device(&d_blob, &d_blob_cap, total, stream, "upload alloc");
+    if (st != CA_OK) return st;
+    char* h = nullptr;
+    if ((st = work_stage.acquire(total, &h)) != CA_OK) return st;
     auto put = [&](size_t o, const void* src, size_t bytes) {
       if (bytes) std::memcpy(h + o, src, bytes);
     };
@@ -182,10 +215,7 @@ struct ca_cache {
     put(o_pptr, W.part_ptr.data(), W.part_ptr.size() * 4);
     put(o_parts, W.parts.data(), W.parts.size() * 4);
     put(o_mg, W.mg_rows.data(), W.mg_rows.size() * 4);
-    if ((e = hipMemcpyAsync(d_blob, h, total, hipMemcpyHostToDevice, stream)) != hipSuccess)
-      return hip_fail(e, "upload copy");
-    if ((e = hipEventRecord(ev[i], stream)) != hipSuccess) return hip_fail(e, "upload record");
-    ev_used[i] = true;
+    if ((st = work_stage.copy(d_blob, total, stream)) != CA_OK) return st;
 
     dw.segs = reinterpret_cast<const ca::CfSeg*>(d_blob + o_segs);
     dw.seg_slots = reinterpret_cast<const int32_t*>(d_blob + o_seg_slots);
@@ -469,6 +499,69 @@ ca_status ca_attention(ca_cache* cache, const void* q, void* o, float scale, voi
   a.cnt = cache->d_cnt;
   hipError_t e = ca::launch_attention(a, cache->dw, s, cache->phase_mask, cache->side);
   if (e != hipSuccess) return hip_fail(e, "ca_attention launch");
+  return CA_OK;
+}
+
+ca_status ca_prefill_attention(ca_cache* cache, int64_t seq_id, const void* q, void* o,
+                               int64_t n_q, float scale, void* stream) {
+  if (!cache) return fail(CA_ERR_INVALID, "ca_prefill_attention: null cache");
+  if (cache->table_only) return fail(CA_ERR_INVALID, "ca_prefill_attention: table-only cache");
+  if (cache->cfg.dtype != CA_FP16)
+    return fail(CA_ERR_INVALID, "ca_prefill_attention: fp16 caches only");
+  const auto& seqs = cache->tree.seqs();
+  auto it = seqs.find(seq_id);
+  if (it == seqs.end()) return fail(CA_ERR_NOT_FOUND, "ca_prefill_attention: unknown sequence");
+  const int64_t L = it->second.length;
+  if (n_q < 0 || n_q > L) return fail(CA_ERR_INVALID, "ca_prefill_attention: need 0 <= n_q <= length");
+  if (n_q == 0) return CA_OK;
+  if (!q || !o) return fail(CA_ERR_INVALID, "ca_prefill_attention: null q/o");
+  if ((reinterpret_cast<uintptr_t>(q) | reinterpret_cast<uintptr_t>(o)) & 15)
+    return fail(CA_ERR_INVALID, "ca_prefill_attention: q/o must be 16-byte aligned");
+  if (!(scale >= 0.f) || std::isinf(scale))
+    return fail(CA_ERR_INVALID, "ca_prefill_attention: bad scale");
+  if (L > INT32_MAX / 2) return fail(CA_ERR_INVALID, "ca_prefill_attention: sequence too long");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+
+  // root -> leaf path: slots and start positions (a chunk may be shorter than c)
+  std::vector<int32_t> path;
+  for (int32_t id = it->second.term; id != ca::ChunkTree::kRoot; id = cache->tree.node(id).parent)
+    path.push_back(id);
+  const int32_t nc = static_cast<int32_t>(path.size());
+  const size_t bytes = (2 * static_cast<size_t>(nc) + 1) * sizeof(int32_t);
+  char* h = nullptr;
+  ca_status st = cache->prefill_stage.acquire(bytes, &h);
+  if (st != CA_OK) return st;
+  int32_t* slot = reinterpret_cast<int32_t*>(h);
+  int32_t* start = slot + nc;
+  int32_t pos = 0;
+  for (int32_t k = 0; k < nc; ++k) {
+    const ca::Node& nd = cache->tree.node(path[nc - 1 - k]);
+    slot[k] = nd.slot;
+    start[k] = pos;
+    pos += static_cast<int32_t>(nd.tokens.size());
+  }
+  start[nc] = pos;
+  if (pos != L) return fail(CA_ERR_INVALID, "ca_prefill_attention: inconsistent path");
+  if ((st = ensure_device(&cache->d_path, &cache->d_path_cap, bytes, s, "prefill path")) != CA_OK)
+    return st;
+  if ((st = cache->prefill_stage.copy(cache->d_path, bytes, s)) != CA_OK) return st;
+
+  ca::PrefillArgs a{};
+  a.H = cache->cfg.num_heads;
+  a.D = cache->cfg.head_dim;
+  a.C = cache->cfg.chunk_size;
+  a.q = q;
+  a.o = o;
+  a.kpool = cache->cfg.k_pool;
+  a.vpool = cache->cfg.v_pool;
+  a.chunk_slot = reinterpret_cast<const int32_t*>(cache->d_path);
+  a.chunk_start = a.chunk_slot + nc;
+  a.n_chunks = nc;
+  a.n_q = static_cast<int>(n_q);
+  const float sc = scale == 0.f ? 1.f / std::sqrt(static_cast<float>(a.D)) : scale;
+  a.qscale = sc * 1.4426950408889634f;
+  hipError_t e = ca::launch_prefill(a, s);
+  if (e != hipSuccess) return hip_fail(e, "ca_prefill_attention launch");
   return CA_OK;
 }
 

@@ -988,6 +988,191 @@ __device__ __forceinline__ void kcf_f32_block(const KcfParams& P, int seg, int z
 }
 
 // ---------------------------------------------------------------------------
+// Prefill with prefix reuse (Section 3.2, prefill paragraph): once a joining
+// sequence's unmatched suffix has been written into the tree, its n_q
+// trailing tokens attend causally to the sequence's whole K/V, read chunk by
+// chunk along the root-to-leaf path. Query i sits at position
+// L - n_q + i and sees positions 0..L - n_q + i.
+//
+// One 256-thread block per (64 queries, head); wavefront w owns queries
+// [16w, 16w+16) of the tile and every token, so the wavefronts never merge.
+// Per chunk (up to 64 tokens), the block stages K as [token][d] and V
+// transposed as [d][token] in LDS, once for all 64 queries; the next chunk's
+// rows are already loading into registers while the current one is used.
+//   S^T = K Q^T  (16x16x32 MFMA: K rows from LDS as A, the wavefront's q rows
+//                 as B, held in registers for the whole call);
+//   causal and chunk-length mask, online softmax per query row (base 2);
+//   O^T += V^T P^T (16x16x16 MFMA: V^T from LDS as A, P^T straight from the
+//                 S^T accumulators as B).
+struct KpfParams {
+  const _Float16* q;            // [n_q][H][D]
+  _Float16* o;                  // [n_q][H][D]
+  const _Float16* kpool;
+  const _Float16* vpool;
+  const int32_t* chunk_slot;    // [n_chunks] path slots, root -> leaf
+  const int32_t* chunk_start;   // [n_chunks + 1] position of each chunk's first token; last = L
+  int n_chunks;
+  int n_q;
+  int H;
+  int C;
+  float qscale;                 // softmax scale * log2(e)
+};
+
+template <int D>
+constexpr int kpf_k_stride() { return D + 8; }   // halves per K row in LDS
+constexpr int kKpfVtStride = 64 + 4;             // halves per V^T row in LDS
+
+// K granule e = tid + 256u: token e / NG, column e % NG (coalesced rows).
+// V granule: token tid % 64, column tid / 64 + 4u (a wavefront covers all 64
+// tokens of one column, so the transposed LDS writes are contiguous). Rows
+// past the chunk's length re-read its last row (their scores are masked).
+template <int D>
+__device__ __forceinline__ void kpf_load_chunk(const KpfParams& P, const _Float16* kbase,
+                                               const _Float16* vbase, size_t slot_stride, int j,
+                                               int tid, u32x4 (&kr)[D / 32], u32x4 (&vr)[D / 32]) {
+  constexpr int NG = D / 8;
+  const int slot = P.chunk_slot[j];
+  const int len = P.chunk_start[j + 1] - P.chunk_start[j];
+  const _Float16* kb = kbase + slot * slot_stride;
+  const _Float16* vb = vbase + slot * slot_stride;
+#pragma unroll
+  for (int u = 0; u < D / 32; ++u) {
+    const int e = tid + 256 * u;
+    kr[u] = *reinterpret_cast<const u32x4*>(kb + static_cast<size_t>(min(e / NG, len - 1)) * D +
+                                            (e % NG) * 8);
+    vr[u] = *reinterpret_cast<const u32x4*>(vb + static_cast<size_t>(min(tid & 63, len - 1)) * D +
+                                            ((tid >> 6) + 4 * u) * 8);
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void kpf_kernel(KpfParams P) {
+  constexpr int KS = D / 32;        // 16x16x32 steps over d
+  constexpr int DT = D / 16;        // 16-wide d tiles of O^T
+  constexpr int NG = D / 8;         // 16-byte granules per token row
+  constexpr int GPT = NG / 4;       // granules of K (and of V) per thread per chunk
+  constexpr int KST = kpf_k_stride<D>();
+  constexpr int VTS = kKpfVtStride;
+  __shared__ __attribute__((aligned(16))) _Float16 k_lds[64 * KST];
+  __shared__ __attribute__((aligned(16))) _Float16 vt_lds[D * VTS];
+
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int l16 = lane & 15, g = lane >> 4;
+  const int h = blockIdx.y;
+  const int H = P.H, C = P.C, n_q = P.n_q;
+  const int L = P.chunk_start[P.n_chunks];
+  const int q0 = static_cast<int>(blockIdx.x) * 64;           // first query of the tile
+  const int qi = q0 + 16 * w + l16;                            // this lane's query row
+  const int pos = L - n_q + qi;                                // its position
+  const int pos_last = L - n_q + min(q0 + 63, n_q - 1);        // last position of the tile
+  const size_t slot_stride = static_cast<size_t>(H) * C * D;
+  const _Float16* kbase = P.kpool + static_cast<size_t>(h) * C * D;
+  const _Float16* vbase = P.vpool + static_cast<size_t>(h) * C * D;
+
+  half8 qf[KS];
+#pragma unroll
+  for (int s = 0; s < KS; ++s) {
+    if (qi < n_q)
+      qf[s] = *reinterpret_cast<const half8*>(P.q + (static_cast<size_t>(qi) * H + h) * D + 32 * s +
+                                              8 * g);
+    else
+      qf[s] = half8{};
+  }
+  float m_run = kNegBig, n_part = 0.f;
+  floatx4 acc[DT];
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt) acc[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  // chunks the tile needs: those starting at or before its last position
+  int n_ch = 0;
+  while (n_ch < P.n_chunks && P.chunk_start[n_ch] <= pos_last) ++n_ch;
+
+  u32x4 kr[GPT], vr[GPT];
+  if (n_ch > 0) kpf_load_chunk<D>(P, kbase, vbase, slot_stride, 0, tid, kr, vr);
+  for (int j = 0; j < n_ch; ++j) {
+    const int c0 = P.chunk_start[j];
+    const int len = P.chunk_start[j + 1] - c0;
+    __syncthreads();  // every wavefront is done with the previous chunk's LDS
+#pragma unroll
+    for (int u = 0; u < GPT; ++u) {
+      const int e = tid + 256 * u;
+      *reinterpret_cast<u32x4*>(k_lds + (e / NG) * KST + (e % NG) * 8) = kr[u];
+      const half8 hv = __builtin_bit_cast(half8, vr[u]);
+      const int tv = tid & 63, col = ((tid >> 6) + 4 * u) * 8;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) vt_lds[(col + k) * VTS + tv] = hv[k];
+    }
+    __syncthreads();
+    if (j + 1 < n_ch)  // in flight while this chunk is used
+      kpf_load_chunk<D>(P, kbase, vbase, slot_stride, j + 1, tid, kr, vr);
+
+    // S^T for the chunk's 64 token slots: tile jt holds tokens 16jt..16jt+15
+    floatx4 sacc[4];
+#pragma unroll
+    for (int jt = 0; jt < 4; ++jt) {
+      sacc[jt] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        const half8 ka = *reinterpret_cast<const half8*>(k_lds + (16 * jt + l16) * KST + 32 * s + 8 * g);
+        sacc[jt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ka, qf[s], sacc[jt], 0, 0, 0);
+      }
+    }
+    // lane holds S^T[token 16jt + 4g + i][row l16]
+    float lmax = kNegBig;
+#pragma unroll
+    for (int jt = 0; jt < 4; ++jt) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int t = 16 * jt + 4 * g + i;
+        const float x = (t < len && c0 + t <= pos) ? sacc[jt][i] * P.qscale : -INFINITY;
+        sacc[jt][i] = x;
+        lmax = fmaxf(lmax, x);
+      }
+    }
+    lmax = fmaxf(lmax, __shfl_xor(lmax, 16));
+    lmax = fmaxf(lmax, __shfl_xor(lmax, 32));
+    const float mn = fmaxf(m_run, lmax);
+    const float alpha = fast_exp2(m_run - mn);
+    m_run = mn;
+    half4 ph[4];
+    float ps = 0.f;
+#pragma unroll
+    for (int jt = 0; jt < 4; ++jt) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        ph[jt][i] = static_cast<_Float16>(fast_exp2(sacc[jt][i] - mn));
+        ps += static_cast<float>(ph[jt][i]);
+      }
+    }
+    n_part = n_part * alpha + ps;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      acc[dt] *= alpha;
+#pragma unroll
+      for (int jt = 0; jt < 4; ++jt) {
+        const half4 va = *reinterpret_cast<const half4*>(vt_lds + (16 * dt + l16) * VTS + 16 * jt + 4 * g);
+        acc[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(va, ph[jt], acc[dt], 0, 0, 0);
+      }
+    }
+  }
+  // row sum over the four lane groups, then O / n
+  float n_row = n_part;
+  n_row += __shfl_xor(n_row, 16);
+  n_row += __shfl_xor(n_row, 32);
+  if (qi < n_q) {
+    const float inv = 1.f / n_row;
+    _Float16* out = P.o + (static_cast<size_t>(qi) * H + h) * D;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      half4 r;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) r[i] = static_cast<_Float16>(acc[dt][i] * inv);
+      *reinterpret_cast<half4*>(out + 16 * dt + 4 * g) = r;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // K/V copies for tree operations.
 
 struct KvJobBatch {
@@ -1182,6 +1367,18 @@ hipError_t launch_attention(const AttnArgs& a, const DevWork& w, hipStream_t s, 
     if (a.D == 64) return launch_all<float, 64>(a, w, s, mask, side);
   }
   return hipErrorInvalidValue;
+}
+
+hipError_t launch_prefill(const PrefillArgs& a, hipStream_t stream) {
+  if (a.n_q <= 0 || a.n_chunks <= 0) return hipSuccess;
+  KpfParams P{static_cast<const _Float16*>(a.q), static_cast<_Float16*>(a.o),
+              static_cast<const _Float16*>(a.kpool), static_cast<const _Float16*>(a.vpool),
+              a.chunk_slot, a.chunk_start, a.n_chunks, a.n_q, a.H, a.C, a.qscale};
+  const dim3 grid((a.n_q + 63) / 64, a.H);
+  if (a.D == 128) kpf_kernel<128><<<grid, 256, 0, stream>>>(P);
+  else if (a.D == 64) kpf_kernel<64><<<grid, 256, 0, stream>>>(P);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
 }
 
 hipError_t launch_kv_jobs(const KvJob* jobs, int n, int dtype, int H, int D, int C, const void* k,

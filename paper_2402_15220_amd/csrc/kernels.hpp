@@ -55,6 +55,22 @@ struct AttnArgs {
 hipError_t launch_attention(const AttnArgs& a, const DevWork& w, hipStream_t stream,
                             int phase_mask, const SideStream& side);
 
+// Causal prefill attention of a sequence's last n_q tokens over its path
+// (fp16 only). chunk_slot/chunk_start are device arrays of the path.
+struct PrefillArgs {
+  int H, D, C;
+  const void* q;
+  void* o;
+  const void* kpool;
+  const void* vpool;
+  const int32_t* chunk_slot;   // [n_chunks]
+  const int32_t* chunk_start;  // [n_chunks + 1]
+  int n_chunks;
+  int n_q;
+  float qscale;  // softmax scale * log2(e)
+};
+hipError_t launch_prefill(const PrefillArgs& a, hipStream_t stream);
+
 // K/V row copies for tree operations (at most kKvJobsPerLaunch per call).
 constexpr int kKvJobsPerLaunch = 64;
 hipError_t launch_kv_jobs(const KvJob* jobs, int n, int dtype, int H, int D, int C,

@@ -1,0 +1,92 @@
+"""GPU parity of prefill with prefix reuse (ca_prefill_attention) against the
+oracle's causal attention over the sequence's whole path."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import prefill_attention
+from paper_2402_15220_amd.binding import ChunkAttnError
+from parity_util import Pair, assert_close, to_dev
+from workloads import make_prefill_join, prefix_keyed_kv
+
+pytestmark = pytest.mark.gpu
+
+
+def test_join_single_prompt_tree_512_new_tokens():
+    """The prefill workload: a 33rd sequence joins the single-shared-prompt tree
+    (1024 shared + 512 unique per row) with the shared prompt plus 512 new
+    tokens; its 512 new tokens attend over 1536 positions."""
+    print("[case] prefill join config 2, 512 new tokens", flush=True)
+    pj = make_prefill_join()
+    wl = pj.static
+    p = Pair(wl.c, wl.H, wl.d, wl.dtype, 400)
+    seg_dev = [(to_dev(s.k), to_dev(s.v)) for s in wl.segments]
+    for s in wl.seqs + [pj.seq]:
+        k, v = s.kv(wl.segments)
+        m = p.insert(s.seq_id, s.tokens(wl.segments), k, v,
+                     dev_k=torch.cat([seg_dev[i][0] for i in s.segs]),
+                     dev_v=torch.cat([seg_dev[i][1] for i in s.segs]))
+    assert m == 1024  # the joining sequence reuses the whole shared prompt
+    p.check_tables()
+    o = p.cache.prefill(pj.seq.seq_id, to_dev(pj.q))
+    torch.cuda.synchronize()
+    ref = prefill_attention(p.tree, pj.seq.seq_id, pj.q, wl.scale)
+    assert_close(o.cpu().numpy(), ref, wl.dtype, "prefill join 512")
+    # the decode call still sees the joined tree correctly
+    q_dec = {s.seq_id: wl.q[s.seq_id] for s in wl.seqs}
+    q_dec[pj.seq.seq_id] = pj.q[-1]
+    od, q, row_seq = p.attention(q_dec)
+    rows = [int(np.nonzero(row_seq == pj.seq.seq_id)[0][0]), 0, len(row_seq) - 1]
+    assert_close(od[rows], p.reference(row_seq, q, 0.0, rows=rows), wl.dtype, "decode after join")
+    # the last prefill query equals the decode row of the joined sequence
+    r = rows[0]
+    assert np.abs(od[r].astype(np.float64) - o[-1].cpu().numpy().astype(np.float64)).max() < 2e-3
+
+
+@pytest.mark.parametrize("case", range(10))
+def test_prefill_random_trees(case):
+    """Shared prefixes that split chunks mid-way, short chunks on the path,
+    n_q from 1 to the whole sequence, both head sizes."""
+    rng = np.random.default_rng(500 + case)
+    c = [1, 3, 4, 7, 16, 64, 5, 64, 16, 2][case]
+    d = [64, 128][case % 2]
+    H = 1 + case % 3
+    print(f"[case] prefill random c={c} d={d} H={H}", flush=True)
+    p = Pair(c, H, d, np.float16, 4096)
+    base = rng.integers(0, 20, int(rng.integers(5, 150))).astype(np.int32)
+    seqs = {}
+    for sid in range(4):
+        cut = int(rng.integers(1, len(base) + 1))
+        tail = rng.integers(20 + 40 * sid, 60 + 40 * sid, int(rng.integers(1, 200))).astype(np.int32)
+        toks = np.concatenate([base[:cut], tail])
+        k, v = prefix_keyed_kv(case, toks, 0, H, d, np.float16)
+        p.insert(sid, toks, k, v)
+        seqs[sid] = toks
+    for sid, toks in seqs.items():
+        L = len(toks)
+        for n_q in sorted({1, min(L, 5), min(L, 63), min(L, 64), min(L, 65), L}):
+            q = rng.standard_normal((n_q, H, d)).astype(np.float16)
+            o = p.cache.prefill(sid, to_dev(q), scale=0.0 if n_q % 2 else 0.2)
+            torch.cuda.synchronize()
+            sc = 1.0 / np.sqrt(d) if n_q % 2 else 0.2
+            ref = prefill_attention(p.tree, sid, q, sc)
+            assert_close(o.cpu().numpy(), ref, np.float16, f"prefill c={c} seq={sid} L={L} n_q={n_q}")
+
+
+def test_prefill_errors_and_noop():
+    p = Pair(4, 2, 64, np.float16, 64)
+    toks = np.arange(10, dtype=np.int32)
+    k, v = prefix_keyed_kv(0, toks, 0, 2, 64, np.float16)
+    p.insert(0, toks, k, v)
+    q = to_dev(np.zeros((11, 2, 64), np.float16))
+    with pytest.raises(ChunkAttnError):
+        p.cache.prefill(0, q)           # more queries than tokens
+    with pytest.raises(ChunkAttnError):
+        p.cache.prefill(5, q[:3])       # unknown sequence
+    o = torch.full((0, 2, 64), 7.0, dtype=torch.float16, device="cuda")
+    p.cache.prefill(0, q[:0], out=o)    # n_q = 0: nothing to do
+    p32 = Pair(4, 2, 64, np.float32, 64)
+    k32, v32 = prefix_keyed_kv(0, toks, 0, 2, 64, np.float32)
+    p32.insert(0, toks, k32, v32)
+    with pytest.raises(ChunkAttnError):
+        p32.cache.prefill(0, to_dev(np.zeros((3, 2, 64), np.float32)))

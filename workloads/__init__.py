@@ -18,5 +18,7 @@ from .synth import (  # noqa: F401
     random_op_script,
     prefix_keyed_kv,
     sweep_tokens,
+    make_prefill_join,
+    PrefillJoin,
     decode_tokens,
 )

@@ -284,6 +284,37 @@ def make_dynamic(config: int = 5, n_steps: int = 64, B: int = 128,
                            segments, seqs, n_steps, churn_steps, int(round(0.1 * B)), rng, redraws)
 
 
+@dataclasses.dataclass
+class PrefillJoin:
+    """A sequence joining a built tree: its prompt repeats an existing shared
+    prompt and adds new tokens, whose K/V and queries are drawn here."""
+
+    static: StaticWorkload   # the tree it joins (its segments grow by one)
+    seq: Sequence            # the joining sequence (shared prompt + new segment)
+    n_new: int
+    q: np.ndarray            # [n_new, H, d] queries of the new tokens
+
+
+def make_prefill_join(n_new: int = 512, config: int = 2) -> PrefillJoin:
+    """The prefill-with-prefix-reuse workload: one more sequence joins the
+    single-shared-prompt tree (config 2 by default) with the 1024-token
+    shared prompt plus ``n_new`` new tokens. Seeded with PCG64(1100 + config)
+    after the static workload's own draws: new tokens (first token distinct
+    from the existing branches), then K and V of the new tokens, then q."""
+    wl = make_static(config)
+    rng = np.random.Generator(np.random.PCG64(1100 + config))
+    prompt = wl.seqs[0].segs[0]
+    firsts = {int(wl.segments[s.segs[-1]].tokens[0]) for s in wl.seqs}
+    t, nr = _draw_tokens(rng, n_new, firsts)
+    wl.redraws += nr
+    k = _draw_values(rng, (n_new, wl.H, wl.d), wl.dtype)
+    v = _draw_values(rng, (n_new, wl.H, wl.d), wl.dtype)
+    q = _draw_values(rng, (n_new, wl.H, wl.d), wl.dtype)
+    wl.segments.append(Segment(t, k, v))
+    seq = Sequence(max(s.seq_id for s in wl.seqs) + 1, [prompt, len(wl.segments) - 1])
+    return PrefillJoin(wl, seq, n_new, q)
+
+
 def sweep_tokens(b: int, n_p: int, n_s: int, seed: int):
     """Token ids of a batch of b prompts of n_p tokens whose first n_s tokens
     are one shared prefix (the paper's microkernel workload). The first
