@@ -40,6 +40,20 @@ typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef _Float16 half4 __attribute__((ext_vector_type(4)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
+typedef __fp16 fp16x4_t __attribute__((__vector_size__(4 * sizeof(__fp16))));
+
+// ds_read_b64_tr_b16: each lane names 4 consecutive halves in LDS; within
+// every 16-lane group, lane i receives element i % 4 of the values named by
+// lanes 4j + i / 4, for j = 0..3. With lane (i, group g) naming row
+// r0 + 4g + i / 4, column c0 + 4 (i % 4) of a row-major [row][col] tile,
+// lane i gets rows r0 + 4g + j, column c0 + i: the 16x16x16 MFMA A operand
+// of the transposed tile, without a transposed copy.
+__device__ __forceinline__ half4 lds_read_tr16(const _Float16* p) {
+  const fp16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4f16(
+      (__attribute__((address_space(3))) fp16x4_t*)(p));
+  return __builtin_bit_cast(half4, v);
+}
+
 constexpr float kNegBig = -FLT_MAX;  // "no score yet": exp2(kNegBig - x) == 0, never NaN
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
@@ -154,7 +168,8 @@ __device__ __forceinline__ void st_dev(float* p, float x) {
 __device__ __forceinline__ float ld_dev(const float* p) {
   return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ void wait_stores() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
+// vmcnt(0): every vector memory access of this wavefront has completed
+__device__ __forceinline__ void wait_stores() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 // Byte offset of element d of partial p, head h in the partial-O workspace.
 __device__ __forceinline__ uint32_t part_off(int p, int H, int D, int h, int d) {
@@ -994,24 +1009,29 @@ __device__ __forceinline__ void kcf_f32_block(const KcfParams& P, int seg, int z
 // chunk along the root-to-leaf path. Query i sits at position
 // L - n_q + i and sees positions 0..L - n_q + i.
 //
-// One 256-thread block per (64 queries, head); wavefront w owns queries
-// [16w, 16w+16) of the tile and every token, so the wavefronts never merge.
-// Per chunk (up to 64 tokens), the block stages K as [token][d] and V
-// transposed as [d][token] in LDS, once for all 64 queries; the next chunk's
-// rows are already loading into registers while the current one is used.
+// One block per (64 queries, head), NGRP groups of four wavefronts. Group
+// k takes chunks k, k+NGRP, ... of the path, so NGRP chunks are in flight
+// per block; inside a group, wavefront w owns queries [16w, 16w+16) of the
+// tile and every token of the group's chunks. Per chunk (up to 64 tokens),
+// the group stages K and V as [token][d] in its LDS tile, once for all 64
+// queries; the group's next chunk is already loading into registers while
+// the current one is used.
 //   S^T = K Q^T  (16x16x32 MFMA: K rows from LDS as A, the wavefront's q rows
 //                 as B, held in registers for the whole call);
 //   causal and chunk-length mask, online softmax per query row (base 2);
-//   O^T += V^T P^T (16x16x16 MFMA: V^T from LDS as A, P^T straight from the
-//                 S^T accumulators as B).
+//   O^T += V^T P^T (16x16x32 MFMA: V^T read from LDS with the transposing
+//                 ds_read_b64_tr_b16 as A, P^T straight from the S^T
+//                 accumulators of two token tiles as B).
+// At the end the groups' states (m, n, O) are folded (Eqn 2) through LDS
+// and group 0 writes o = O / n.
 struct KpfParams {
   const _Float16* q;            // [n_q][H][D]
   _Float16* o;                  // [n_q][H][D]
   const _Float16* kpool;
   const _Float16* vpool;
-  const int32_t* chunk_slot;    // [n_chunks] path slots, root -> leaf
-  const int32_t* chunk_start;   // [n_chunks + 1] position of each chunk's first token; last = L
-  int n_chunks;
+  int n_chunks;                 // chunk_slot [n_chunks] path slots root -> leaf, chunk_start
+                                // [n_chunks + 1] first position of each chunk (last = L):
+                                // kernel arguments of their own
   int n_q;
   int H;
   int C;
@@ -1019,48 +1039,56 @@ struct KpfParams {
 };
 
 template <int D>
-constexpr int kpf_k_stride() { return D + 8; }   // halves per K row in LDS
-constexpr int kKpfVtStride = 64 + 4;             // halves per V^T row in LDS
+constexpr int kpf_k_stride() { return D + 8; }   // halves per K (and V) row in LDS
 
 // K granule e = tid + 256u: token e / NG, column e % NG (coalesced rows).
 // V granule: token tid % 64, column tid / 64 + 4u (a wavefront covers all 64
 // tokens of one column, so the transposed LDS writes are contiguous). Rows
 // past the chunk's length re-read its last row (their scores are masked).
+// One chunk's K and V rows for the group's 256 threads: granule e = tid +
+// 256u is token e / (D/8), 16-byte column e % (D/8) (coalesced rows). Rows
+// past the chunk's length re-read its last row (their scores are masked).
 template <int D>
-__device__ __forceinline__ void kpf_load_chunk(const KpfParams& P, const _Float16* kbase,
-                                               const _Float16* vbase, size_t slot_stride, int j,
-                                               int tid, u32x4 (&kr)[D / 32], u32x4 (&vr)[D / 32]) {
+__device__ __forceinline__ void kpf_load_chunk(const _Float16* kbase, const _Float16* vbase,
+                                               size_t slot_stride, int slot, int len, int tid,
+                                               u32x4 (&kr)[D / 32], u32x4 (&vr)[D / 32]) {
   constexpr int NG = D / 8;
-  const int slot = P.chunk_slot[j];
-  const int len = P.chunk_start[j + 1] - P.chunk_start[j];
   const _Float16* kb = kbase + slot * slot_stride;
   const _Float16* vb = vbase + slot * slot_stride;
 #pragma unroll
   for (int u = 0; u < D / 32; ++u) {
     const int e = tid + 256 * u;
-    kr[u] = *reinterpret_cast<const u32x4*>(kb + static_cast<size_t>(min(e / NG, len - 1)) * D +
-                                            (e % NG) * 8);
-    vr[u] = *reinterpret_cast<const u32x4*>(vb + static_cast<size_t>(min(tid & 63, len - 1)) * D +
-                                            ((tid >> 6) + 4 * u) * 8);
+    const size_t off = static_cast<size_t>(min(e / NG, len - 1)) * D + (e % NG) * 8;
+    kr[u] = *reinterpret_cast<const u32x4*>(kb + off);
+    vr[u] = *reinterpret_cast<const u32x4*>(vb + off);
   }
 }
 
 template <int D>
-__global__ __launch_bounds__(256) void kpf_kernel(KpfParams P) {
+constexpr int kpf_tile_bytes() { return 2 * 64 * kpf_k_stride<D>() * 2; }
+
+template <int D, int NGRP>
+__global__ __launch_bounds__(256 * NGRP) void kpf_kernel(KpfParams P,
+                                                          const int32_t* __restrict__ chunk_slot,
+                                                          const int32_t* __restrict__ chunk_start) {
   constexpr int KS = D / 32;        // 16x16x32 steps over d
   constexpr int DT = D / 16;        // 16-wide d tiles of O^T
   constexpr int NG = D / 8;         // 16-byte granules per token row
   constexpr int GPT = NG / 4;       // granules of K (and of V) per thread per chunk
   constexpr int KST = kpf_k_stride<D>();
-  constexpr int VTS = kKpfVtStride;
-  __shared__ __attribute__((aligned(16))) _Float16 k_lds[64 * KST];
-  __shared__ __attribute__((aligned(16))) _Float16 vt_lds[D * VTS];
+  constexpr int TB = kpf_tile_bytes<D>();
+  static_assert(NGRP == 1 || TB * NGRP >= (NGRP - 1) * 64 * (D + 2) * 4, "merge buffer");
+  __shared__ __attribute__((aligned(16))) char lds[TB * NGRP];
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, w = (tid >> 6) & 3;
+  const int grp = __builtin_amdgcn_readfirstlane(tid >> 8);  // uniform: chunk indices stay scalar
+  const int gtid = tid & 255;  // thread index inside the group
   const int l16 = lane & 15, g = lane >> 4;
+  _Float16* k_lds = reinterpret_cast<_Float16*>(lds + grp * TB);
+  _Float16* v_lds = k_lds + 64 * KST;
   const int h = blockIdx.y;
   const int H = P.H, C = P.C, n_q = P.n_q;
-  const int L = P.chunk_start[P.n_chunks];
+  const int L = chunk_start[P.n_chunks];
   const int q0 = static_cast<int>(blockIdx.x) * 64;           // first query of the tile
   const int qi = q0 + 16 * w + l16;                            // this lane's query row
   const int pos = L - n_q + qi;                                // its position
@@ -1078,33 +1106,54 @@ __global__ __launch_bounds__(256) void kpf_kernel(KpfParams P) {
     else
       qf[s] = half8{};
   }
+  // q has arrived before any chunk load is issued, so the MFMAs inside the
+  // loop never wait on vector memory (the next chunk's loads stay in flight)
+  wait_stores();
   float m_run = kNegBig, n_part = 0.f;
   floatx4 acc[DT];
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) acc[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  // chunks the tile needs: those starting at or before its last position
+  // Chunks the tile needs: those starting at or before its last position
+  // (starts ascend); 64 starts per load, one per lane.
+  const int nc = P.n_chunks;
   int n_ch = 0;
-  while (n_ch < P.n_chunks && P.chunk_start[n_ch] <= pos_last) ++n_ch;
-
-  u32x4 kr[GPT], vr[GPT];
-  if (n_ch > 0) kpf_load_chunk<D>(P, kbase, vbase, slot_stride, 0, tid, kr, vr);
-  for (int j = 0; j < n_ch; ++j) {
-    const int c0 = P.chunk_start[j];
-    const int len = P.chunk_start[j + 1] - c0;
+  for (int b = 0; b < nc; b += 64) {
+    const int st = b + lane < nc ? chunk_start[b + lane] : 0x7fffffff;
+    const unsigned long long m = __ballot(st <= pos_last);
+    n_ch += __popcll(m);
+    if (m != ~0ull) break;
+  }
+  // Per-chunk metadata comes through the scalar cache (uniform index,
+  // read-only arguments), so no metadata load ever waits behind the chunk
+  // rows in flight. Two register buffers per group: chunk j's rows arrive
+  // while chunk j - NGRP is used, and chunk j + NGRP's loads are issued
+  // before chunk j is used, so two chunks per group are in flight.
+  auto issue = [&](u32x4 (&kr)[GPT], u32x4 (&vr)[GPT], int j) {
+    const int st = chunk_start[j];
+    kpf_load_chunk<D>(kbase, vbase, slot_stride, chunk_slot[j], chunk_start[j + 1] - st, gtid, kr,
+                      vr);
+  };
+  auto step = [&](u32x4 (&kr)[GPT], u32x4 (&vr)[GPT], int j) {
+    const bool have = j < n_ch;
     __syncthreads();  // every wavefront is done with the previous chunk's LDS
+    if (have) {
 #pragma unroll
-    for (int u = 0; u < GPT; ++u) {
-      const int e = tid + 256 * u;
-      *reinterpret_cast<u32x4*>(k_lds + (e / NG) * KST + (e % NG) * 8) = kr[u];
-      const half8 hv = __builtin_bit_cast(half8, vr[u]);
-      const int tv = tid & 63, col = ((tid >> 6) + 4 * u) * 8;
-#pragma unroll
-      for (int k = 0; k < 8; ++k) vt_lds[(col + k) * VTS + tv] = hv[k];
+      for (int u = 0; u < GPT; ++u) {
+        const int e = gtid + 256 * u;
+        *reinterpret_cast<u32x4*>(k_lds + (e / NG) * KST + (e % NG) * 8) = kr[u];
+        *reinterpret_cast<u32x4*>(v_lds + (e / NG) * KST + (e % NG) * 8) = vr[u];
+      }
     }
+    // The chunk these registers load next. Past the end they reload the last
+    // chunk: every step issues the same loads, so the wait before each LDS
+    // write covers exactly the registers it needs on every path.
+    const int jn = min(j + 2 * NGRP, n_ch - 1);
     __syncthreads();
-    if (j + 1 < n_ch)  // in flight while this chunk is used
-      kpf_load_chunk<D>(P, kbase, vbase, slot_stride, j + 1, tid, kr, vr);
+    issue(kr, vr, jn);  // in flight while this chunk and the next are used
+    if (!have) return;
+    const int c0 = chunk_start[j];
+    const int len = chunk_start[j + 1] - c0;
 
     // S^T for the chunk's 64 token slots: tile jt holds tokens 16jt..16jt+15
     floatx4 sacc[4];
@@ -1145,29 +1194,83 @@ __global__ __launch_bounds__(256) void kpf_kernel(KpfParams P) {
       }
     }
     n_part = n_part * alpha + ps;
+    // O^T += V^T P^T over 32 tokens per 16x16x32 MFMA: lane group g's
+    // 8-token K-slice is tokens 4g..4g+3 of tiles 2p and 2p+1 (any token
+    // order works as long as both operands share it), which is exactly what
+    // the lane holds of P^T, and two transposing reads fetch the V^T side.
+    half8 pb[2];
+#pragma unroll
+    for (int p2 = 0; p2 < 2; ++p2)
+      pb[p2] = __builtin_shufflevector(ph[2 * p2], ph[2 * p2 + 1], 0, 1, 2, 3, 4, 5, 6, 7);
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
       acc[dt] *= alpha;
 #pragma unroll
-      for (int jt = 0; jt < 4; ++jt) {
-        const half4 va = *reinterpret_cast<const half4*>(vt_lds + (16 * dt + l16) * VTS + 16 * jt + 4 * g);
-        acc[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(va, ph[jt], acc[dt], 0, 0, 0);
+      for (int p2 = 0; p2 < 2; ++p2) {
+        const _Float16* vp = v_lds + (32 * p2 + 4 * g + (l16 >> 2)) * KST + 16 * dt + 4 * (l16 & 3);
+        const half4 v0 = lds_read_tr16(vp);             // tokens 32p + 4g + j
+        const half4 v1 = lds_read_tr16(vp + 16 * KST);  // tokens 32p + 16 + 4g + j
+        const half8 va = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
+        acc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(va, pb[p2], acc[dt], 0, 0, 0);
       }
     }
+  };
+  u32x4 kr0[GPT], vr0[GPT], kr1[GPT], vr1[GPT];
+  if (n_ch > 0) {
+    issue(kr0, vr0, min(grp, n_ch - 1));
+    issue(kr1, vr1, min(grp + NGRP, n_ch - 1));
   }
-  // row sum over the four lane groups, then O / n
+  // the same even number of steps in every group (steps past the end only
+  // keep the barriers and the load pattern)
+  const int steps = 2 * ((n_ch + 2 * NGRP - 1) / (2 * NGRP));
+  for (int i = 0; i < steps; i += 2) {
+    step(kr0, vr0, grp + i * NGRP);
+    step(kr1, vr1, grp + (i + 1) * NGRP);
+  }
+  // row sums over the four lane groups
   float n_row = n_part;
   n_row += __shfl_xor(n_row, 16);
   n_row += __shfl_xor(n_row, 32);
+  if constexpr (NGRP > 1) {
+    // groups 1.. hand their (m, n, O) to group 0 through LDS (Eqn 2)
+    float* ob = reinterpret_cast<float*>(lds);                    // [NGRP-1][64][D]
+    float* mb = ob + (NGRP - 1) * 64 * D;                          // [NGRP-1][64][2]
+    const int r = 16 * w + l16;
+    __syncthreads();  // the tiles are free
+    if (grp > 0) {
+      float* o_ = ob + ((grp - 1) * 64 + r) * D;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+        *reinterpret_cast<floatx4*>(o_ + 16 * dt + 4 * g) = acc[dt];
+      if (g == 0) {
+        mb[((grp - 1) * 64 + r) * 2] = m_run;
+        mb[((grp - 1) * 64 + r) * 2 + 1] = n_row;
+      }
+    }
+    __syncthreads();
+    if (grp > 0) return;
+#pragma unroll
+    for (int k = 1; k < NGRP; ++k) {
+      const float mo = mb[((k - 1) * 64 + r) * 2], no = mb[((k - 1) * 64 + r) * 2 + 1];
+      const float M = fmaxf(m_run, mo);
+      const float ws = fast_exp2(m_run - M), wo = fast_exp2(mo - M);
+      const float* o_ = ob + ((k - 1) * 64 + r) * D;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+        acc[dt] = acc[dt] * ws + *reinterpret_cast<const floatx4*>(o_ + 16 * dt + 4 * g) * wo;
+      n_row = n_row * ws + no * wo;
+      m_run = M;
+    }
+  }
   if (qi < n_q) {
     const float inv = 1.f / n_row;
     _Float16* out = P.o + (static_cast<size_t>(qi) * H + h) * D;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
-      half4 r;
+      half4 r4;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) r[i] = static_cast<_Float16>(acc[dt][i] * inv);
-      *reinterpret_cast<half4*>(out + 16 * dt + 4 * g) = r;
+      for (int i = 0; i < 4; ++i) r4[i] = static_cast<_Float16>(acc[dt][i] * inv);
+      *reinterpret_cast<half4*>(out + 16 * dt + 4 * g) = r4;
     }
   }
 }
@@ -1373,10 +1476,13 @@ hipError_t launch_prefill(const PrefillArgs& a, hipStream_t stream) {
   if (a.n_q <= 0 || a.n_chunks <= 0) return hipSuccess;
   KpfParams P{static_cast<const _Float16*>(a.q), static_cast<_Float16*>(a.o),
               static_cast<const _Float16*>(a.kpool), static_cast<const _Float16*>(a.vpool),
-              a.chunk_slot, a.chunk_start, a.n_chunks, a.n_q, a.H, a.C, a.qscale};
+              a.n_chunks, a.n_q, a.H, a.C, a.qscale};
+  constexpr int kGroups = 2;
   const dim3 grid((a.n_q + 63) / 64, a.H);
-  if (a.D == 128) kpf_kernel<128><<<grid, 256, 0, stream>>>(P);
-  else if (a.D == 64) kpf_kernel<64><<<grid, 256, 0, stream>>>(P);
+  if (a.D == 128)
+    kpf_kernel<128, kGroups><<<grid, 256 * kGroups, 0, stream>>>(P, a.chunk_slot, a.chunk_start);
+  else if (a.D == 64)
+    kpf_kernel<64, kGroups><<<grid, 256 * kGroups, 0, stream>>>(P, a.chunk_slot, a.chunk_start);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }
