@@ -338,7 +338,8 @@ def dynamic_run():
     o = torch.empty_like(q_rows)
     torch.cuda.synchronize()
     t_gen = time.perf_counter() - t_gen
-    up0 = cache.stats()["uploads"]
+    st0 = cache.stats()
+    up0, pa0 = st0["uploads"], st0["patches"]
 
     att_us, step_us, rows = [], [], []
     for st, added, k, v, q in dev_steps:
@@ -363,7 +364,8 @@ def dynamic_run():
         step_us.append((time.perf_counter() - t0) * 1e6)
         att_us.append(a.elapsed_time(b) * 1e3)
         rows.append(n)
-    up = cache.stats()["uploads"] - up0
+    st1 = cache.stats()
+    up, pa = st1["uploads"] - up0, st1["patches"] - pa0
     cache.close()
     del cache, seg_dev, dev_steps
     torch.cuda.empty_cache()
@@ -371,7 +373,7 @@ def dynamic_run():
             "attention_us_mean": float(np.mean(att_us)), "attention_us_median": float(np.median(att_us)),
             "step_us_mean": float(np.mean(step_us)), "step_us_median": float(np.median(step_us)),
             "tok_per_s": float(sum(rows) / (sum(att_us) * 1e-6)),
-            "context_uploads": int(up), "setup_s": t_gen}
+            "context_uploads": int(up), "context_patched_in_place": int(pa), "setup_s": t_gen}
 
 
 def cpu_baseline(wl, rows, seconds):

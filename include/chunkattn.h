@@ -207,11 +207,16 @@ ca_status ca_prefill_attention(ca_cache* cache, int64_t seq_id, const void* q, v
 ca_status ca_export_tables(const ca_cache* cache, ca_tables* out);
 
 /* Counters for tests and reports: number of kernel-context uploads so far,
- * slots in use, total slots, the attention schedule (see ca_set_tuning) and
- * the chunk-first segment size of the current kernel context. Any pointer
- * may be NULL. */
+ * slots in use, total slots, the attention schedule (see ca_set_tuning), the
+ * chunk-first segment size of the current kernel context, and how many
+ * context updates were done in place (decode growth: new private chunks at
+ * the end of paths patch the per-row lists instead of rebuilding them,
+ * Section 3.3). Any pointer may be NULL. With CA_CHECK_PATCH=1 in the
+ * environment at ca_create, every in-place update is compared with a full
+ * rebuild and a difference makes this call return INVALID. */
 ca_status ca_stats(const ca_cache* cache, int64_t* uploads, int64_t* slots_used,
-                   int64_t* slots_total, int32_t* schedule, int32_t* seg_chunks);
+                   int64_t* slots_total, int32_t* schedule, int32_t* seg_chunks,
+                   int64_t* patches);
 
 /* Tuning and per-phase measurement (schedules change speed, not results).
  *   seg_chunks   shared chunks per chunk-first work item (1..64; 0 keeps the

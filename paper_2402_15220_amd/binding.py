@@ -86,7 +86,7 @@ def load():
         "ca_attention": [vp, vp, vp, ctypes.c_float, vp, ctypes.c_size_t, vp],
         "ca_prefill_attention": [vp, i64, vp, vp, i64, ctypes.c_float, vp],
         "ca_export_tables": [vp, ctypes.POINTER(CaTables)],
-        "ca_stats": [vp, _P64, _P64, _P64, ctypes.POINTER(i32), ctypes.POINTER(i32)],
+        "ca_stats": [vp, _P64, _P64, _P64, ctypes.POINTER(i32), ctypes.POINTER(i32), _P64],
         "ca_set_tuning": [vp, i32, i32, i32, i32],
     }
     for name, args in sig.items():
@@ -216,12 +216,12 @@ def ca_export_tables(h) -> dict:
 
 
 def ca_stats(h):
-    u, s, t = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+    u, s, t, p = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
     sc, sg = ctypes.c_int32(), ctypes.c_int32()
     _check(load().ca_stats(h, ctypes.byref(u), ctypes.byref(s), ctypes.byref(t), ctypes.byref(sc),
-                           ctypes.byref(sg)))
+                           ctypes.byref(sg), ctypes.byref(p)))
     return dict(uploads=u.value, slots_used=s.value, slots_total=t.value, schedule=sc.value,
-                seg_chunks=sg.value)
+                seg_chunks=sg.value, patches=p.value)
 
 
 def ca_set_tuning(h, seg_chunks=0, split_chunks=-1, phase_mask=0, schedule=-1):

@@ -129,6 +129,9 @@ struct ca_cache {
   ca::Tables tables;
   ca::WorkLists work;
   bool work_valid = false;
+  int64_t patches = 0;        // in-place work-list updates so far
+  bool check_patches = false; // compare every patch with a rebuild (CA_CHECK_PATCH=1)
+  std::string patch_error;    // set when such a comparison failed
   int32_t seg_chunks = 0;  // 0: automatic
   int32_t num_cus = 256;
   int32_t split_chunks = 0;
@@ -166,11 +169,31 @@ struct ca_cache {
 
   size_t esize() const { return cfg.dtype == CA_FP16 ? 2 : 4; }
 
+  // Work lists for the current tree. Decode growth (new private chunks at
+  // the end of paths) patches them in place (Section 3.3's context stays
+  // valid except for those rows' chunk lists); anything else rebuilds the
+  // tables and the work lists. `tables` keeps row_seq valid either way.
   void ensure_work() {
     if (work_valid && !tree.dirty()) return;
-    ca::build_tables(tree, &tables);
-    ca::build_work(tree, tables, seg_chunks, split_chunks, schedule != 0, cfg.num_heads, num_cus,
-                   &work);
+    bool patched = false;
+    if (work_valid && tree.private_growth_only() && split_chunks <= 0 && !patch_error.size())
+      patched = ca::patch_work(tree, &work);
+    if (patched) {
+      ++patches;
+      if (check_patches) {
+        ca::Tables t;
+        ca::WorkLists full;
+        ca::build_tables(tree, &t);
+        ca::build_work(tree, t, seg_chunks, split_chunks, schedule != 0, cfg.num_heads, num_cus,
+                       &full);
+        const char* d = ca::same_work(work, full);
+        if (*d) patch_error = std::string("work-list patch differs from a rebuild: ") + d;
+      }
+    } else {
+      ca::build_tables(tree, &tables);
+      ca::build_work(tree, tables, seg_chunks, split_chunks, schedule != 0, cfg.num_heads, num_cus,
+                     &work);
+    }
     work_valid = true;
     dw_valid = false;
     tree.clear_dirty();
@@ -325,6 +348,7 @@ ca_status ca_create(const ca_config* cfg, ca_cache** out) {
   c->seg_chunks = std::max(0, env_int("CA_CF_SEG", 0));
   c->split_chunks = env_int("CA_SPLIT", 0);
   c->schedule = std::min(3, std::max(0, env_int("CA_SCHEDULE", 2)));
+  c->check_patches = env_int("CA_CHECK_PATCH", 0) != 0;
   if (!c->table_only) {
     int dev = 0, cus = 0;
     if (hipGetDevice(&dev) == hipSuccess &&
@@ -616,8 +640,11 @@ ca_status ca_set_tuning(ca_cache* cache, int32_t seg_chunks, int32_t split_chunk
 }
 
 ca_status ca_stats(const ca_cache* cache, int64_t* uploads, int64_t* slots_used,
-                   int64_t* slots_total, int32_t* schedule, int32_t* seg_chunks) {
+                   int64_t* slots_total, int32_t* schedule, int32_t* seg_chunks,
+                   int64_t* patches) {
   if (!cache) return fail(CA_ERR_INVALID, "ca_stats: null cache");
+  if (!cache->patch_error.empty()) return fail(CA_ERR_INVALID, cache->patch_error);
+  if (patches) *patches = cache->patches;
   if (uploads) *uploads = cache->uploads;
   if (slots_used) *slots_used = cache->tree.pool().in_use();
   if (slots_total) *slots_total = cache->tree.pool().capacity();

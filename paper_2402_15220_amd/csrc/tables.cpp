@@ -211,6 +211,71 @@ void build_work(const ChunkTree& tree, const Tables& T, int32_t seg_chunks, int3
     return a.ce - a.cb > b.ce - b.cb;
   });
   W.n_parts = part;
+  W.row_of_seq.clear();
+  for (int64_t r = 0; r < B; ++r) W.row_of_seq[T.row_seq[r]] = static_cast<int32_t>(r);
+  W.item_of_row.assign(B, -1);
+  std::vector<int32_t> pieces(B, 0);
+  for (size_t i = 0; i < W.items.size(); ++i) {
+    const int32_t r = W.items[i].row;
+    if (pieces[r]++ == 0) W.item_of_row[r] = static_cast<int32_t>(i);
+    else W.item_of_row[r] = -1;
+  }
+}
+
+bool patch_work(const ChunkTree& tree, WorkLists* w) {
+  WorkLists& W = *w;
+  const auto& grown = tree.grown();
+  for (const auto& g : grown) {  // check first: all or nothing
+    auto it = W.row_of_seq.find(g.first);
+    if (it == W.row_of_seq.end() || W.item_of_row[it->second] < 0) return false;
+  }
+  for (const auto& g : grown) {
+    const int32_t r = W.row_of_seq.at(g.first);
+    const int32_t self = W.item_of_row[r];
+    const int32_t at = W.items[self].ce;  // end of the row's private list
+    W.priv_slot.insert(W.priv_slot.begin() + at, tree.node(g.second).slot);
+    for (auto& it : W.items)
+      if (it.cb >= at && &it != &W.items[self]) {
+        ++it.cb;
+        ++it.ce;
+      }
+    ++W.items[self].ce;
+  }
+  // keep longest-first; rows keep their items
+  std::vector<int32_t> order(W.items.size());
+  for (size_t i = 0; i < order.size(); ++i) order[i] = static_cast<int32_t>(i);
+  std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) {
+    return W.items[a].ce - W.items[a].cb > W.items[b].ce - W.items[b].cb;
+  });
+  std::vector<SfItem> sorted(W.items.size());
+  for (size_t i = 0; i < order.size(); ++i) sorted[i] = W.items[order[i]];
+  W.items.swap(sorted);
+  for (size_t i = 0; i < W.items.size(); ++i) W.item_of_row[W.items[i].row] = static_cast<int32_t>(i);
+  return true;
+}
+
+const char* same_work(const WorkLists& a, const WorkLists& b) {
+  if (a.seg_slots != b.seg_slots || a.segs.size() != b.segs.size()) return "segments";
+  for (size_t i = 0; i < a.segs.size(); ++i)
+    if (a.segs[i].slot_off != b.segs[i].slot_off || a.segs[i].n_chunks != b.segs[i].n_chunks ||
+        a.segs[i].row_begin != b.segs[i].row_begin || a.segs[i].row_end != b.segs[i].row_end ||
+        a.segs[i].part_base != b.segs[i].part_base)
+      return "segments";
+  if (a.part_ptr != b.part_ptr || a.parts != b.parts || a.mg_rows != b.mg_rows ||
+      a.n_parts != b.n_parts)
+    return "partial lists";
+  if (a.items.size() != b.items.size()) return "item count";
+  auto key = [](const WorkLists& w) {
+    std::vector<std::vector<int32_t>> k(w.item_of_row.size());
+    for (const auto& it : w.items) {
+      auto& v = k[it.row];
+      v.push_back(it.out_part);
+      v.insert(v.end(), w.priv_slot.begin() + it.cb, w.priv_slot.begin() + it.ce);
+    }
+    return k;
+  };
+  if (key(a) != key(b)) return "sequence-first items";
+  return "";
 }
 
 }  // namespace ca

@@ -3,6 +3,7 @@
 #pragma once
 
 #include <cstdint>
+#include <unordered_map>
 #include <vector>
 
 #include "tree.hpp"
@@ -55,9 +56,26 @@ struct WorkLists {
   int64_t n_parts = 0;
   int32_t max_seg_rows = 0;
   int32_t seg_chunks = 0;  // segment size used
+  // for in-place updates: row of each live sequence, and the index in
+  // `items` of each row's single item (-1: none or several pieces)
+  std::unordered_map<int64_t, int32_t> row_of_seq;
+  std::vector<int32_t> item_of_row;
 };
 
 void build_work(const ChunkTree& tree, const Tables& t, int32_t seg_chunks, int32_t split_chunks,
                 bool partial_items, int32_t num_heads, int32_t num_cus, WorkLists* out);
+
+// Bring work lists built for an earlier tree up to date when the only
+// structural changes since were new private chunks at the end of sequences'
+// paths (tree.grown()): row order, shared runs, segments and partials are
+// unchanged, and each new chunk's slot is appended to its row's private list
+// (the rows after it shift by one). Returns false, changing nothing, when a
+// row cannot be patched this way (no single item for the row).
+bool patch_work(const ChunkTree& tree, WorkLists* w);
+
+// Compare two work lists up to the order of sequence-first items: every row
+// has the same private slots and item kind, segments and partial lists are
+// equal. Empty string when they agree, else what differs.
+const char* same_work(const WorkLists& a, const WorkLists& b);
 
 }  // namespace ca

@@ -99,7 +99,7 @@ int32_t ChunkTree::split(int32_t x, int32_t p, std::vector<KvJob>* jobs) {
     jobs->push_back({1, X.slot, p, slot, 0, L - p});
     jobs->push_back({2, 0, 0, X.slot, p, 0});
   }
-  dirty_ = true;
+  mark_structural();
   return x;
 }
 
@@ -139,7 +139,7 @@ Err ChunkTree::insert(int64_t sid, const int32_t* tokens, int64_t n, std::vector
   auto& terms = nodes_[term].terminals;
   terms.insert(std::lower_bound(terms.begin(), terms.end(), sid), sid);
   seqs_[sid] = {term, n};
-  dirty_ = true;
+  mark_structural();
   return Err::ok;
 }
 
@@ -162,6 +162,11 @@ Err ChunkTree::extend_impl(int64_t sid, const int32_t* tokens, int64_t n, int32_
                          static_cast<int32_t>(f)});
     }
     end = new_chain(t, tokens, n, f, row_base, jobs);
+    if (end != t) {
+      const size_t first = grown_.size();
+      for (int32_t x = end; x != t; x = nodes_[x].parent) grown_.emplace_back(sid, x);
+      std::reverse(grown_.begin() + static_cast<std::ptrdiff_t>(first), grown_.end());
+    }
   } else {
     const Descent d = descend(t, tokens, n, 0);
     const int64_t need = (d.split_node >= 0 ? 1 : 0) + chunks_for(n - d.pos, c_);
@@ -170,6 +175,7 @@ Err ChunkTree::extend_impl(int64_t sid, const int32_t* tokens, int64_t n, int32_
     int32_t cur = d.cur;
     if (d.split_node >= 0) cur = split(d.split_node, d.split_at, jobs);
     end = new_chain(cur, tokens, n, d.pos, row_base, jobs);
+    if (end != t) mark_structural();  // the sequence leaves a shared chunk
   }
   if (end != t) {
     auto& old = nodes_[t].terminals;
@@ -234,7 +240,7 @@ Err ChunkTree::remove(int64_t sid) {
     }
     x = parent;
   }
-  dirty_ = true;
+  mark_structural();
   return Err::ok;
 }
 

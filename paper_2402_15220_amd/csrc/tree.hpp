@@ -89,7 +89,16 @@ class ChunkTree {
   // Structure changed since the flag was last cleared (a chunk appeared or
   // disappeared, a chunk was split, a sequence joined or left).
   bool dirty() const { return dirty_; }
-  void clear_dirty() { dirty_ = false; }
+  void clear_dirty() {
+    dirty_ = false;
+    private_growth_only_ = true;
+    grown_.clear();
+  }
+  // Since the flag was last cleared, the only structural changes were new
+  // chunks below sequences' private last chunks (decode growth); grown()
+  // lists them as (sequence, node) in creation order.
+  bool private_growth_only() const { return private_growth_only_; }
+  const std::vector<std::pair<int64_t, int32_t>>& grown() const { return grown_; }
 
   const std::vector<Node>& nodes() const { return nodes_; }
   const Node& node(int32_t id) const { return nodes_[id]; }
@@ -126,7 +135,14 @@ class ChunkTree {
   std::vector<Node> nodes_;
   std::vector<int32_t> free_nodes_;
   std::unordered_map<int64_t, SeqInfo> seqs_;
+  void mark_structural() {
+    dirty_ = true;
+    private_growth_only_ = false;
+  }
+
   bool dirty_ = true;
+  bool private_growth_only_ = false;
+  std::vector<std::pair<int64_t, int32_t>> grown_;
 };
 
 }  // namespace ca

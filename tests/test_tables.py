@@ -221,3 +221,69 @@ def test_work_lists_follow_lazy_context_rule():
     B.ca_append_batch(h, [0, 1], [7, 7])   # fills the private chunks [5], [6]
     assert B.ca_workspace_size(h) == ws0
     B.ca_destroy(h)
+
+
+def _checked_cache(*args):
+    """A table-only cache that compares every in-place context update with a
+    full rebuild (a difference makes ca_stats raise)."""
+    old = os.environ.get("CA_CHECK_PATCH")
+    os.environ["CA_CHECK_PATCH"] = "1"
+    try:
+        return B.ca_create(*args)
+    finally:
+        if old is None:
+            del os.environ["CA_CHECK_PATCH"]
+        else:
+            os.environ["CA_CHECK_PATCH"] = old
+
+
+def test_decode_growth_updates_context_in_place():
+    """Section 3.3 (lazy context): decode growth that only adds private chunks
+    patches the per-row lists; each patch equals a full rebuild, through 64
+    decode steps with churn (where the context is rebuilt)."""
+    _lib_or_skip()
+    wl = make_dynamic()
+    h = _checked_cache(wl.c, wl.H, wl.d, B.CA_FP16, 1 << 16)
+    for s in wl.seqs:
+        B.ca_insert(h, s.seq_id, s.tokens(wl.segments))
+    B.ca_seq_order(h)
+    for st in wl.steps():
+        if st.churn:
+            for sid in st.churn.removed:
+                B.ca_remove(h, sid)
+            for s in st.churn.added:
+                B.ca_insert(h, s.seq_id, s.tokens(wl.segments))
+        B.ca_append_batch(h, st.live, st.tokens)
+        B.ca_seq_order(h)          # brings the context up to date
+        B.ca_stats(h)              # raises if a patch differed from a rebuild
+    assert B.ca_stats(h)["patches"] >= 40
+    B.ca_destroy(h)
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_random_growth_patches_match_rebuild(seed):
+    """Small trees, small chunks: appends and extends that grow private chains,
+    mixed with inserts, splits and removals (which rebuild)."""
+    _lib_or_skip()
+    c = 1 + seed % 4
+    h = _checked_cache(c, 1, 64, B.CA_FP16, 1 << 20)
+    live = set()
+    for op in random_op_script(seed, n_ops=120, alphabet=3, max_len=2 * c + 3):
+        if op[0] in ("extend", "remove") and op[1] not in live:
+            continue
+        if op[0] == "insert":
+            B.ca_insert(h, op[1], op[2])
+            live.add(op[1])
+        elif op[0] == "extend":
+            B.ca_extend(h, op[1], op[2])
+        elif op[0] == "append":
+            ids = [s for s in op[1] if s in live]
+            if not ids:
+                continue
+            B.ca_append_batch(h, ids, op[2][:len(ids)])
+        elif op[0] == "remove":
+            B.ca_remove(h, op[1])
+            live.discard(op[1])
+        B.ca_seq_order(h)
+        B.ca_stats(h)
+    B.ca_destroy(h)
