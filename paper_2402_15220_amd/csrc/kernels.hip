@@ -683,27 +683,57 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
     my_slot = P.seg_slots[sg.slot_off + lane];
     my_len = P.slot_len[my_slot];
   }
-  int j = 0, t0 = 0;
-  int slot = __builtin_amdgcn_readlane(my_slot, 0);
-  int len = __builtin_amdgcn_readlane(my_len, 0);
+  // Software pipeline without extra registers: the next block's K rows are
+  // requested as soon as this block's S^T MFMAs have read theirs, and its V
+  // rows as soon as this block's V rows are in LDS, so each block's loads
+  // overlap the previous block's softmax and P.V; every iteration issues the
+  // same loads, so each wait covers only the rows it needs.
+  // Unconditional loads: rows past a block's end re-read its last row (valid
+  // and finite); their scores are masked to -inf below, so P = 0.
   const int ktok = 16 * w + l16;  // this lane's K row within a block
-  while (true) {
-    const int nt = min(64, len - t0);
-    const _Float16* kb = kpool + slot * slot_stride + static_cast<size_t>(t0) * D;
-    const _Float16* vb = vpool + slot * slot_stride + static_cast<size_t>(t0) * D;
-    // Unconditional loads: rows past the block's end re-read its last row
-    // (valid and finite); their scores are masked to -inf below, so P = 0.
-    half8 kf[KS];
+  half8 kf[KS];
+  uint4 vr[NVL];
+  auto load_k = [&](int sl, int tb, int ln) {
+    const int ntb = min(64, ln - tb);
+    const _Float16* kb = kpool + sl * slot_stride + static_cast<size_t>(tb) * D;
 #pragma unroll
     for (int s = 0; s < KS; ++s)
-      kf[s] = *reinterpret_cast<const half8*>(kb + static_cast<size_t>(min(ktok, nt - 1)) * D +
+      kf[s] = *reinterpret_cast<const half8*>(kb + static_cast<size_t>(min(ktok, ntb - 1)) * D +
                                               32 * s + 8 * g);
-    uint4 vr[NVL];
+  };
+  auto load_v = [&](int sl, int tb, int ln) {
+    const int ntb = min(64, ln - tb);
+    const _Float16* vb = vpool + sl * slot_stride + static_cast<size_t>(tb) * D;
 #pragma unroll
     for (int i = 0; i < NVL; ++i) {
       const int tl = lane / GPR + TPL * i;
-      vr[i] = *reinterpret_cast<const uint4*>(vb + static_cast<size_t>(min(16 * w + tl, nt - 1)) * D +
+      vr[i] = *reinterpret_cast<const uint4*>(vb + static_cast<size_t>(min(16 * w + tl, ntb - 1)) * D +
                                               (lane % GPR) * 8);
+    }
+  };
+  int j = 0, t0 = 0;
+  int slot = __builtin_amdgcn_readlane(my_slot, 0);
+  int len = __builtin_amdgcn_readlane(my_len, 0);
+  load_k(slot, t0, len);
+  load_v(slot, t0, len);
+  while (true) {
+    const int nt = min(64, len - t0);
+    // the block after this one; after the last block, the loads re-read one
+    // row of it (every lane the same row: two cache lines, never used)
+    int nj = j, nt0 = t0 + 64, nslot = slot, nlen = len;
+    if (nt0 >= len) {
+      nt0 = 0;
+      ++nj;
+      if (nj < sg.n_chunks) {
+        nslot = __builtin_amdgcn_readlane(my_slot, nj);
+        nlen = __builtin_amdgcn_readlane(my_len, nj);
+      }
+    }
+    const bool more = nj < sg.n_chunks;
+    if (!more) {
+      nt0 = len - 1;
+      nslot = slot;
+      nlen = len;
     }
     floatx4 sacc[NRT];
 #pragma unroll
@@ -715,6 +745,7 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
           sacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(kf[s], qf[t][s], sacc[t], 0, 0, 0);
       }
     }
+    load_k(nslot, nt0, nlen);
     half4 ph[NRT];
     float alpha[NRT];
 #pragma unroll
@@ -749,6 +780,7 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
       dst[0] = make_uint2(vr[i].x, vr[i].y);
       dst[1] = make_uint2(vr[i].z, vr[i].w);
     }
+    load_v(nslot, nt0, nlen);
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
       half4 va;
@@ -762,15 +794,11 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
         }
       }
     }
-    // next block
-    t0 += 64;
-    if (t0 >= len) {
-      t0 = 0;
-      ++j;
-      if (j >= sg.n_chunks) break;
-      slot = __builtin_amdgcn_readlane(my_slot, j);
-      len = __builtin_amdgcn_readlane(my_len, j);
-    }
+    if (!more) break;
+    j = nj;
+    t0 = nt0;
+    slot = nslot;
+    len = nlen;
   }
 
   // Merge the four wavefront states per row: common max, rescaled sums.
