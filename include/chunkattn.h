@@ -65,14 +65,23 @@ typedef enum { CA_FP16 = 0, CA_FP32 = 1 } ca_dtype;
  *   head_dim    d in {64, 128}
  *   dtype       element type of K, V, q and o
  *   num_slots   number of chunk slots in each pool (>= 1)
- *   k_pool, v_pool  caller-owned device buffers, each at least
- *               num_slots * H * c * d * sizeof(dtype) bytes, 16-byte aligned,
- *               layout [slot][head][c][d] (row-major). The library writes
- *               only rows it owns and never frees them.
+ *   k_pool, v_pool  caller-owned device buffers, 16-byte aligned. The K rows
+ *               of chunk slot s, head h are the c*d contiguous elements at
+ *               k_pool + s*slot_stride + h*head_stride (row-major [c][d]);
+ *               V likewise from v_pool. The library writes only rows it
+ *               owns and never frees the pools.
  *               Both NULL: a table-only cache that keeps the tree and its
  *               tables but stores no K/V (k/v arguments must then be NULL and
  *               ca_attention is refused). Used to exercise the host tree
  *               without a GPU.
+ *   slot_stride, head_stride  in elements; 0 means the dense layout
+ *               [slot][head][c][d] (head_stride = c*d, slot_stride = H*c*d).
+ *               head_stride >= c*d, slot_stride >= (H-1)*head_stride + c*d,
+ *               both multiples of 16 bytes; K and V tiles must not overlap.
+ *               Each pool spans (num_slots-1)*slot_stride + (H-1)*head_stride
+ *               + c*d elements. Example: the interleaved layout
+ *               [slot][head][K|V][c][d] in one buffer is v_pool = k_pool + c*d,
+ *               head_stride = 2*c*d, slot_stride = 2*H*c*d.
  */
 typedef struct {
   int32_t chunk_size;
@@ -82,6 +91,8 @@ typedef struct {
   int64_t num_slots;
   void* k_pool;
   void* v_pool;
+  int64_t slot_stride;
+  int64_t head_stride;
 } ca_config;
 
 /*

@@ -44,7 +44,8 @@ class CaConfig(ctypes.Structure):
     _fields_ = [("chunk_size", ctypes.c_int32), ("num_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("dtype", ctypes.c_int32),
                 ("num_slots", ctypes.c_int64), ("k_pool", ctypes.c_void_p),
-                ("v_pool", ctypes.c_void_p)]
+                ("v_pool", ctypes.c_void_p), ("slot_stride", ctypes.c_int64),
+                ("head_stride", ctypes.c_int64)]
 
 
 _P32 = ctypes.POINTER(ctypes.c_int32)
@@ -119,8 +120,10 @@ def ca_last_error() -> str:
     return load().ca_last_error().decode()
 
 
-def ca_create(chunk_size, num_heads, head_dim, dtype, num_slots, k_pool=None, v_pool=None):
-    cfg = CaConfig(chunk_size, num_heads, head_dim, dtype, num_slots, k_pool, v_pool)
+def ca_create(chunk_size, num_heads, head_dim, dtype, num_slots, k_pool=None, v_pool=None,
+              slot_stride=0, head_stride=0):
+    cfg = CaConfig(chunk_size, num_heads, head_dim, dtype, num_slots, k_pool, v_pool, slot_stride,
+                   head_stride)
     h = ctypes.c_void_p()
     _check(load().ca_create(ctypes.byref(cfg), ctypes.byref(h)))
     return h

@@ -13,12 +13,16 @@ _DT = {torch.float16: B.CA_FP16, torch.float32: B.CA_FP32}
 class Cache:
     """A prefix-tree chunked KV cache on one GPU (or table-only on the host).
 
-    Pools are allocated here with torch (layout [slot][head][c][d]) and lent
-    to the library; q/o rows follow ``seq_order()``.
+    Pools are allocated here with torch and lent to the library; q/o rows
+    follow ``seq_order()``. ``layout="split"`` (default) uses two buffers
+    [slot][head][c][d]; ``"interleaved"`` keeps each chunk-head's K and V
+    tiles adjacent in one buffer [slot][head][K|V][c][d] (strided pools).
+    ``k_pool``/``v_pool`` are [slot][head][c][d] views either way.
     """
 
     def __init__(self, chunk_size: int, num_heads: int, head_dim: int, num_slots: int,
-                 dtype=torch.float16, device="cuda", table_only: bool = False):
+                 dtype=torch.float16, device="cuda", table_only: bool = False,
+                 layout: str = "split"):
         self.c, self.H, self.d = chunk_size, num_heads, head_dim
         self.dtype = dtype
         self.num_slots = num_slots
@@ -26,12 +30,23 @@ class Cache:
         if table_only:
             self.k_pool = self.v_pool = None
             self.h = B.ca_create(chunk_size, num_heads, head_dim, _DT[dtype], num_slots)
-        else:
+        elif layout == "interleaved":
+            self.kv_pool = torch.empty((num_slots, num_heads, 2, chunk_size, head_dim), dtype=dtype,
+                                       device=device)
+            self.k_pool = self.kv_pool[:, :, 0]
+            self.v_pool = self.kv_pool[:, :, 1]
+            tile = chunk_size * head_dim
+            self.h = B.ca_create(chunk_size, num_heads, head_dim, _DT[dtype], num_slots,
+                                 self.k_pool.data_ptr(), self.v_pool.data_ptr(),
+                                 slot_stride=2 * num_heads * tile, head_stride=2 * tile)
+        elif layout == "split":
             shape = (num_slots, num_heads, chunk_size, head_dim)
             self.k_pool = torch.empty(shape, dtype=dtype, device=device)
             self.v_pool = torch.empty(shape, dtype=dtype, device=device)
             self.h = B.ca_create(chunk_size, num_heads, head_dim, _DT[dtype], num_slots,
                                  self.k_pool.data_ptr(), self.v_pool.data_ptr())
+        else:
+            raise ValueError(f"unknown layout {layout!r}")
         self._ws = None
 
     # -- helpers -----------------------------------------------------------

@@ -303,8 +303,8 @@ struct ca_cache {
       if (batch.empty()) return CA_OK;
       hipError_t e = ca::launch_kv_jobs(batch.data(), static_cast<int>(batch.size()),
                                         cfg.dtype == CA_FP16 ? 0 : 1, cfg.num_heads, cfg.head_dim,
-                                        cfg.chunk_size, k, v, cfg.k_pool, cfg.v_pool, d_slot_len,
-                                        stream);
+                                        cfg.chunk_size, cfg.slot_stride, cfg.head_stride, k, v,
+                                        cfg.k_pool, cfg.v_pool, d_slot_len, stream);
       batch.clear();
       touched.clear();
       if (e != hipSuccess) return hip_fail(e, "kv copy launch");
@@ -342,7 +342,18 @@ ca_status ca_create(const ca_config* cfg, ca_cache** out) {
     return fail(CA_ERR_INVALID, "ca_create: give both pools or neither");
   if ((reinterpret_cast<uintptr_t>(cfg->k_pool) | reinterpret_cast<uintptr_t>(cfg->v_pool)) & 15)
     return fail(CA_ERR_INVALID, "ca_create: pools must be 16-byte aligned");
-  ca_cache* c = new (std::nothrow) ca_cache(*cfg);
+  ca_config norm = *cfg;
+  {
+    const int64_t tile = static_cast<int64_t>(cfg->chunk_size) * cfg->head_dim;
+    const int64_t es = cfg->dtype == CA_FP16 ? 2 : 4;
+    if (norm.head_stride == 0) norm.head_stride = tile;
+    if (norm.slot_stride == 0) norm.slot_stride = cfg->num_heads * norm.head_stride;
+    if (norm.head_stride < tile || norm.slot_stride < (cfg->num_heads - 1) * norm.head_stride + tile)
+      return fail(CA_ERR_INVALID, "ca_create: strides overlap tiles");
+    if ((norm.head_stride * es) % 16 || (norm.slot_stride * es) % 16)
+      return fail(CA_ERR_INVALID, "ca_create: strides must be multiples of 16 bytes");
+  }
+  ca_cache* c = new (std::nothrow) ca_cache(norm);
   if (!c) return fail(CA_ERR_INVALID, "ca_create: out of host memory");
   c->table_only = cfg->k_pool == nullptr;
   c->seg_chunks = std::max(0, env_int("CA_CF_SEG", 0));
@@ -508,6 +519,8 @@ ca_status ca_attention(ca_cache* cache, const void* q, void* o, float scale, voi
   a.o = o;
   a.kpool = cache->cfg.k_pool;
   a.vpool = cache->cfg.v_pool;
+  a.ss = cache->cfg.slot_stride;
+  a.hs = cache->cfg.head_stride;
   a.slot_len = cache->d_slot_len;
   const size_t np = static_cast<size_t>(cache->work.n_parts);
   const size_t o_bytes = np * a.H * a.D * 4;
@@ -578,6 +591,8 @@ ca_status ca_prefill_attention(ca_cache* cache, int64_t seq_id, const void* q, v
   a.o = o;
   a.kpool = cache->cfg.k_pool;
   a.vpool = cache->cfg.v_pool;
+  a.ss = cache->cfg.slot_stride;
+  a.hs = cache->cfg.head_stride;
   a.chunk_slot = reinterpret_cast<const int32_t*>(cache->d_path);
   a.chunk_start = a.chunk_slot + nc;
   a.n_chunks = nc;

@@ -302,6 +302,7 @@ struct KsfParams {
   void* o;
   const void* kpool;
   const void* vpool;
+  int64_t ss, hs;  // pool strides of a slot and of a head (elements)
   const int32_t* slot_len;
   const SfItem* items;
   const int32_t* priv_slot;
@@ -354,9 +355,9 @@ __device__ __forceinline__ void ksf_block(const KsfParams& P, int item, int h, c
 #pragma unroll
   for (int j = 0; j < EPL; ++j) acc[j] = 0.f;
 
-  const T* kpool = static_cast<const T*>(P.kpool) + static_cast<size_t>(h) * C * D + sub * EPL;
-  const T* vpool = static_cast<const T*>(P.vpool) + static_cast<size_t>(h) * C * D + sub * EPL;
-  const size_t slot_stride = static_cast<size_t>(H) * C * D;
+  const T* kpool = static_cast<const T*>(P.kpool) + h * P.hs + sub * EPL;
+  const T* vpool = static_cast<const T*>(P.vpool) + h * P.hs + sub * EPL;
+  const size_t slot_stride = static_cast<size_t>(P.ss);
   const int tok_off = w * TPW + tr;  // this lane's token within a step (u = 0)
 
   // Loads are unconditional (no branches, so the compiler can count them):
@@ -544,6 +545,7 @@ struct KcfParams {
   const void* q;
   const void* kpool;
   const void* vpool;
+  int64_t ss, hs;  // pool strides of a slot and of a head (elements)
   const int32_t* slot_len;
   const CfSeg* segs;
   const int32_t* seg_slots;
@@ -649,9 +651,9 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
   if (nrows <= 0) return;
   const int nrt = (nrows + 15) / 16;
   const _Float16* q = static_cast<const _Float16*>(P.q);
-  const _Float16* kpool = static_cast<const _Float16*>(P.kpool) + static_cast<size_t>(h) * C * D;
-  const _Float16* vpool = static_cast<const _Float16*>(P.vpool) + static_cast<size_t>(h) * C * D;
-  const size_t slot_stride = static_cast<size_t>(H) * C * D;
+  const _Float16* kpool = static_cast<const _Float16*>(P.kpool) + h * P.hs;
+  const _Float16* vpool = static_cast<const _Float16*>(P.vpool) + h * P.hs;
+  const size_t slot_stride = static_cast<size_t>(P.ss);
 
   half8 qf[NRT][KS];
 #pragma unroll
@@ -916,7 +918,7 @@ __device__ __forceinline__ void kcf_f32_block(const KcfParams& P, int seg, int z
   for (int ci = 0; ci < sg.n_chunks; ++ci) {
     const int slot = P.seg_slots[sg.slot_off + ci];
     const int len = P.slot_len[slot];
-    const size_t base = (static_cast<size_t>(slot) * H + h) * static_cast<size_t>(C) * D;
+    const size_t base = static_cast<size_t>(slot) * P.ss + h * P.hs;
     const float* kb = kpool + base;
     const float* vb = vpool + base;
     for (int t0 = 0; t0 < len; t0 += 64) {
@@ -1057,6 +1059,7 @@ struct KpfParams {
   _Float16* o;                  // [n_q][H][D]
   const _Float16* kpool;
   const _Float16* vpool;
+  int64_t ss, hs;               // pool strides of a slot and of a head (elements)
   int n_chunks;                 // chunk_slot [n_chunks] path slots root -> leaf, chunk_start
                                 // [n_chunks + 1] first position of each chunk (last = L):
                                 // kernel arguments of their own
@@ -1121,9 +1124,9 @@ __global__ __launch_bounds__(256 * NGRP) void kpf_kernel(KpfParams P,
   const int qi = q0 + 16 * w + l16;                            // this lane's query row
   const int pos = L - n_q + qi;                                // its position
   const int pos_last = L - n_q + min(q0 + 63, n_q - 1);        // last position of the tile
-  const size_t slot_stride = static_cast<size_t>(H) * C * D;
-  const _Float16* kbase = P.kpool + static_cast<size_t>(h) * C * D;
-  const _Float16* vbase = P.vpool + static_cast<size_t>(h) * C * D;
+  const size_t slot_stride = static_cast<size_t>(P.ss);
+  const _Float16* kbase = P.kpool + h * P.hs;
+  const _Float16* vbase = P.vpool + h * P.hs;
 
   half8 qf[KS];
 #pragma unroll
@@ -1313,13 +1316,14 @@ struct KvJobBatch {
 
 __global__ __launch_bounds__(256) void kkv_kernel(KvJobBatch b, const char* k, const char* v,
                                                   char* kpool, char* vpool, int32_t* slot_len,
-                                                  int H, int row_bytes, int C) {
+                                                  int H, int row_bytes, int64_t ss_bytes,
+                                                  int64_t hs_bytes) {
   const KvJob j = b.job[blockIdx.x];
   const int h = blockIdx.y;
   if (j.kind != 2) {
     const int units = row_bytes / 16;
-    const size_t dst = ((static_cast<size_t>(j.dst_slot) * H + h) * C + j.dst_pos) *
-                       static_cast<size_t>(row_bytes);
+    const size_t dst = static_cast<size_t>(j.dst_slot) * ss_bytes + h * hs_bytes +
+                       static_cast<size_t>(j.dst_pos) * row_bytes;
     const char *sk, *sv;
     size_t src, stride;
     if (j.kind == 0) {
@@ -1330,7 +1334,8 @@ __global__ __launch_bounds__(256) void kkv_kernel(KvJobBatch b, const char* k, c
     } else {
       sk = kpool;
       sv = vpool;
-      src = ((static_cast<size_t>(j.src) * H + h) * C + j.src_pos) * static_cast<size_t>(row_bytes);
+      src = static_cast<size_t>(j.src) * ss_bytes + h * hs_bytes +
+            static_cast<size_t>(j.src_pos) * row_bytes;
       stride = row_bytes;
     }
     for (int i = threadIdx.x; i < j.n * units; i += blockDim.x) {
@@ -1452,10 +1457,10 @@ hipError_t launch_all(const AttnArgs& a, const DevWork& w, hipStream_t s, int ma
                       const SideStream& side) {
   TppParams P;
   const bool counting = w.schedule >= 2;  // the last contributor finishes each row
-  P.cf = KcfParams{a.q, a.kpool, a.vpool, a.slot_len, w.segs, w.seg_slots, a.ws_o,
+  P.cf = KcfParams{a.q, a.kpool, a.vpool, a.ss, a.hs, a.slot_len, w.segs, w.seg_slots, a.ws_o,
                    reinterpret_cast<float2*>(a.ws_ml), a.ws_o_bytes, a.H, a.C, a.qscale,
                    counting ? a.cnt : nullptr, a.o, w.part_ptr, w.parts};
-  P.sf = KsfParams{a.q, a.o, a.kpool, a.vpool, a.slot_len, w.items, w.priv_slot, w.part_ptr,
+  P.sf = KsfParams{a.q, a.o, a.kpool, a.vpool, a.ss, a.hs, a.slot_len, w.items, w.priv_slot, w.part_ptr,
                    w.parts, a.ws_o, reinterpret_cast<float2*>(a.ws_ml), a.ws_o_bytes, a.H, a.C,
                    a.qscale, counting ? a.cnt : nullptr};
   // At most 16 or 32 covered rows per chunk-first block; wider runs take
@@ -1503,8 +1508,8 @@ hipError_t launch_attention(const AttnArgs& a, const DevWork& w, hipStream_t s, 
 hipError_t launch_prefill(const PrefillArgs& a, hipStream_t stream) {
   if (a.n_q <= 0 || a.n_chunks <= 0) return hipSuccess;
   KpfParams P{static_cast<const _Float16*>(a.q), static_cast<_Float16*>(a.o),
-              static_cast<const _Float16*>(a.kpool), static_cast<const _Float16*>(a.vpool),
-              a.n_chunks, a.n_q, a.H, a.C, a.qscale};
+              static_cast<const _Float16*>(a.kpool), static_cast<const _Float16*>(a.vpool), a.ss,
+              a.hs, a.n_chunks, a.n_q, a.H, a.C, a.qscale};
   constexpr int kGroups = 2;
   const dim3 grid((a.n_q + 63) / 64, a.H);
   if (a.D == 128)
@@ -1515,18 +1520,21 @@ hipError_t launch_prefill(const PrefillArgs& a, hipStream_t stream) {
   return hipGetLastError();
 }
 
-hipError_t launch_kv_jobs(const KvJob* jobs, int n, int dtype, int H, int D, int C, const void* k,
-                          const void* v, void* kpool, void* vpool, int32_t* slot_len,
-                          hipStream_t stream) {
+hipError_t launch_kv_jobs(const KvJob* jobs, int n, int dtype, int H, int D, int C, int64_t ss,
+                          int64_t hs, const void* k, const void* v, void* kpool, void* vpool,
+                          int32_t* slot_len, hipStream_t stream) {
   if (n <= 0) return hipSuccess;
   if (n > kKvJobsPerLaunch) return hipErrorInvalidValue;
   KvJobBatch b;
   b.n = n;
   for (int i = 0; i < n; ++i) b.job[i] = jobs[i];
   const int row_bytes = D * (dtype == 0 ? 2 : 4);
+  const int64_t es = dtype == 0 ? 2 : 4;
+  (void)C;
   kkv_kernel<<<dim3(n, H), 256, 0, stream>>>(b, static_cast<const char*>(k),
                                              static_cast<const char*>(v), static_cast<char*>(kpool),
-                                             static_cast<char*>(vpool), slot_len, H, row_bytes, C);
+                                             static_cast<char*>(vpool), slot_len, H, row_bytes,
+                                             ss * es, hs * es);
   return hipGetLastError();
 }
 

@@ -41,6 +41,7 @@ struct AttnArgs {
   void* o;
   const void* kpool;
   const void* vpool;
+  int64_t ss, hs;  // pool strides of a slot and of a head (elements)
   const int32_t* slot_len;
   float* ws_o;   // [n_parts][H][D]
   float* ws_ml;  // [n_parts][H][2] (running max in log2 units, sum)
@@ -63,6 +64,7 @@ struct PrefillArgs {
   void* o;
   const void* kpool;
   const void* vpool;
+  int64_t ss, hs;              // pool strides of a slot and of a head (elements)
   const int32_t* chunk_slot;   // [n_chunks]
   const int32_t* chunk_start;  // [n_chunks + 1]
   int n_chunks;
@@ -73,8 +75,8 @@ hipError_t launch_prefill(const PrefillArgs& a, hipStream_t stream);
 
 // K/V row copies for tree operations (at most kKvJobsPerLaunch per call).
 constexpr int kKvJobsPerLaunch = 64;
-hipError_t launch_kv_jobs(const KvJob* jobs, int n, int dtype, int H, int D, int C,
-                          const void* k, const void* v, void* kpool, void* vpool,
+hipError_t launch_kv_jobs(const KvJob* jobs, int n, int dtype, int H, int D, int C, int64_t ss,
+                          int64_t hs, const void* k, const void* v, void* kpool, void* vpool,
                           int32_t* slot_len, hipStream_t stream);
 
 }  // namespace ca

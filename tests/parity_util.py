@@ -51,9 +51,9 @@ def assert_close(o, ref, dtype, what=""):
 class Pair:
     """The same cache on both sides: the HIP library and the oracle."""
 
-    def __init__(self, c, H, d, dtype, num_slots, oracle_kv=True):
+    def __init__(self, c, H, d, dtype, num_slots, oracle_kv=True, layout="split"):
         self.dtype = np.dtype(dtype)
-        self.cache = Cache(c, H, d, num_slots, dtype=TORCH_DT[self.dtype])
+        self.cache = Cache(c, H, d, num_slots, dtype=TORCH_DT[self.dtype], layout=layout)
         self.tree = OracleTree(c=c, with_kv=oracle_kv)
         self.H, self.d, self.c = H, d, c
 

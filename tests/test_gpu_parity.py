@@ -22,9 +22,9 @@ def _gpu():
     yield
 
 
-def _static_pair(wl, slack=16):
+def _static_pair(wl, slack=16, layout="split"):
     nodes = sum(-(-len(s) // wl.c) for s in wl.segments)  # aligned configs: one chunk set per segment
-    p = Pair(wl.c, wl.H, wl.d, wl.dtype, nodes + slack)
+    p = Pair(wl.c, wl.H, wl.d, wl.dtype, nodes + slack, layout=layout)
     seg_dev = [(to_dev(s.k), to_dev(s.v)) for s in wl.segments]
     for s in wl.seqs:
         toks = s.tokens(wl.segments)
@@ -35,11 +35,13 @@ def _static_pair(wl, slack=16):
     return p
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4])
-def test_static_config(cfg):
-    print(f"[case] static config {cfg}", flush=True)
+@pytest.mark.parametrize("cfg,layout", [(1, "split"), (2, "split"), (3, "split"), (4, "split"),
+                                        (1, "interleaved"), (2, "interleaved")])
+def test_static_config(cfg, layout):
+    """Full-size static trees; K/V pools split (default) and interleaved."""
+    print(f"[case] static config {cfg} layout={layout}", flush=True)
     wl = make_static(cfg)
-    p = _static_pair(wl)
+    p = _static_pair(wl, layout=layout)
     tb = p.check_tables()
     p.check_pool(max_nodes=48)
     o, q, row_seq = p.attention({s.seq_id: wl.q[s.seq_id] for s in wl.seqs})
@@ -118,7 +120,7 @@ def test_random_trees(seed):
     dtype = [np.float16, np.float32][(seed // 2) % 2]
     H = 1 + seed % 3
     print(f"[case] random tree seed={seed} c={c} d={d} H={H} dtype={np.dtype(dtype).name}", flush=True)
-    p = Pair(c, H, d, dtype, 4096)
+    p = Pair(c, H, d, dtype, 4096, layout="interleaved" if seed % 5 == 2 else "split")
     full = {}
     qrng = np.random.default_rng(1000 + seed)
     ops = random_op_script(seed, n_ops=50, alphabet=3, max_len=max(12, 2 * c + 3))

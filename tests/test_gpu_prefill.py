@@ -46,13 +46,14 @@ def test_join_single_prompt_tree_512_new_tokens():
 @pytest.mark.parametrize("case", range(10))
 def test_prefill_random_trees(case):
     """Shared prefixes that split chunks mid-way, short chunks on the path,
-    n_q from 1 to the whole sequence, both head sizes."""
+    n_q from 1 to the whole sequence, both head sizes and both pool layouts."""
     rng = np.random.default_rng(500 + case)
     c = [1, 3, 4, 7, 16, 64, 5, 64, 16, 2][case]
     d = [64, 128][case % 2]
     H = 1 + case % 3
-    print(f"[case] prefill random c={c} d={d} H={H}", flush=True)
-    p = Pair(c, H, d, np.float16, 4096)
+    layout = "interleaved" if case % 4 == 3 else "split"
+    print(f"[case] prefill random c={c} d={d} H={H} layout={layout}", flush=True)
+    p = Pair(c, H, d, np.float16, 4096, layout=layout)
     base = rng.integers(0, 20, int(rng.integers(5, 150))).astype(np.int32)
     seqs = {}
     for sid in range(4):

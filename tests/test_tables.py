@@ -197,7 +197,10 @@ def test_error_paths_leave_state_unchanged():
 
 
 @pytest.mark.parametrize("bad", [
-    dict(chunk_size=0), dict(num_heads=0), dict(head_dim=96), dict(dtype=7), dict(num_slots=0)])
+    dict(chunk_size=0), dict(num_heads=0), dict(head_dim=96), dict(dtype=7), dict(num_slots=0),
+    dict(head_stride=4 * 64 - 8),                                  # a tile is c*d = 256 elements
+    dict(num_heads=4, head_stride=4 * 64, slot_stride=3 * 4 * 64),  # slots would overlap
+    dict(head_stride=4 * 64 + 4)])                                 # not a multiple of 16 bytes
 def test_create_rejects_bad_config(bad):
     _lib_or_skip()
     cfg = dict(chunk_size=4, num_heads=1, head_dim=64, dtype=B.CA_FP16, num_slots=8)
