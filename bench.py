@@ -53,7 +53,7 @@ def _parse():
     ap.add_argument("--split", type=int, default=-1, help="sequence-first split (-1: library default)")
     ap.add_argument("--schedule", type=int, default=-1,
                     help="0 sequential, 1 fused + merge launch, 2 fused with in-kernel merge, "
-                         "3 two streams (-1: library default)")
+                         "3 two streams, 4 partial-free serial reduction (-1: library default)")
     return ap.parse_args()
 
 

@@ -242,7 +242,14 @@ ca_status ca_stats(const ca_cache* cache, int64_t* uploads, int64_t* slots_used,
  *                launch; 3: the two phases as concurrent kernels,
  *                chunk-first on a stream owned by the cache that forks from
  *                and joins back into the caller's stream, rows finished as
- *                in 2. -1 keeps the current value.
+ *                in 2; 4: partial-free reduction (Section 3.3, further
+ *                optimizations): the workspace holds one accumulator per
+ *                (sequence, head) instead of one partial per (segment, row,
+ *                head); chunk-first segments fold into it in path order, one
+ *                launch per position along the path (a run of shared chunks
+ *                is one segment unless seg_chunks is set), then the
+ *                sequence-first launch folds it and writes o; split_chunks
+ *                is ignored. -1 keeps the current value.
  *   split_chunks private chunks per sequence-first work item; rows with more
  *                private chunks are split and merged by the merge epilogue
  *                (0 disables splitting, -1 keeps the current value).

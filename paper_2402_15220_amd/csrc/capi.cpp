@@ -185,14 +185,14 @@ struct ca_cache {
         ca::WorkLists full;
         ca::build_tables(tree, &t);
         ca::build_work(tree, t, seg_chunks, split_chunks, schedule != 0, cfg.num_heads, num_cus,
-                       &full);
+                       &full, schedule == 4);
         const char* d = ca::same_work(work, full);
         if (*d) patch_error = std::string("work-list patch differs from a rebuild: ") + d;
       }
     } else {
       ca::build_tables(tree, &tables);
       ca::build_work(tree, tables, seg_chunks, split_chunks, schedule != 0, cfg.num_heads, num_cus,
-                     &work);
+                     &work, schedule == 4);
     }
     work_valid = true;
     dw_valid = false;
@@ -252,6 +252,8 @@ struct ca_cache {
     dw.mg_rows = reinterpret_cast<const int32_t*>(d_blob + o_mg);
     dw.n_mg = static_cast<int32_t>(W.mg_rows.size());
     dw.schedule = schedule;
+    dw.seg_group_ptr = W.seg_group_ptr.data();
+    dw.n_seg_groups = W.seg_group_ptr.empty() ? 0 : static_cast<int32_t>(W.seg_group_ptr.size()) - 1;
     dw_valid = true;
     ++uploads;
     return CA_OK;
@@ -358,7 +360,7 @@ ca_status ca_create(const ca_config* cfg, ca_cache** out) {
   c->table_only = cfg->k_pool == nullptr;
   c->seg_chunks = std::max(0, env_int("CA_CF_SEG", 0));
   c->split_chunks = env_int("CA_SPLIT", 0);
-  c->schedule = std::min(3, std::max(0, env_int("CA_SCHEDULE", 2)));
+  c->schedule = std::min(4, std::max(0, env_int("CA_SCHEDULE", 2)));
   c->check_patches = env_int("CA_CHECK_PATCH", 0) != 0;
   if (!c->table_only) {
     int dev = 0, cus = 0;
@@ -632,7 +634,7 @@ ca_status ca_set_tuning(ca_cache* cache, int32_t seg_chunks, int32_t split_chunk
                         int32_t phase_mask, int32_t schedule) {
   if (!cache) return fail(CA_ERR_INVALID, "ca_set_tuning: null cache");
   if (seg_chunks < -1 || seg_chunks > 64 || split_chunks < -1 || phase_mask < 0 || phase_mask > 7 ||
-      schedule < -1 || schedule > 3)
+      schedule < -1 || schedule > 4)
     return fail(CA_ERR_INVALID, "ca_set_tuning: value out of range");
   bool rebuild = false;
   if (seg_chunks == -1) seg_chunks = 0;  // automatic

@@ -854,12 +854,41 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
   }
   // write the segment's partial (O, m, n) for every covered row
   const size_t pbase = static_cast<size_t>(sg.part_base + (rb - sg.row_begin));
+  const bool fold = sg.pad0 != 0;
+  if (fold) {
+    // serial reduction: fold into the row's accumulator (Eqn 2), which an
+    // earlier launch wrote; per-row factors go through mbuf / nbuf (free now)
+    if (w == 0 && g == 0) {
+#pragma unroll
+      for (int t = 0; t < NRT; ++t) {
+        const int r = 16 * t + l16;
+        if (r < nrows) {
+          const float* pml = reinterpret_cast<const float*>(P.ws_ml + (pbase + r) * H + h);
+          const float mp = ld_dev(pml), np = ld_dev(pml + 1);
+          const float mx = fmaxf(Mrow[t], mp);
+          const float x = fast_exp2(Mrow[t] - mx), y = fast_exp2(mp - mx);
+          mbuf[r] = x;
+          nbuf[r] = y;
+          Mrow[t] = mx;
+          Nrow[t] = x * Nrow[t] + y * np;
+        }
+      }
+    }
+    __syncthreads();
+  }
   {
     const __amdgpu_buffer_rsrc_t rs = part_rsrc(P.ws_o, P.o_bytes);
     for (int e = tid; e < nrows * (D / 4); e += 256) {
       const int r = e / (D / 4), d = 4 * (e % (D / 4));
-      const float4 v = *reinterpret_cast<const float4*>(obuf + r * OS + d);
-      st_dev4(rs, part_off(static_cast<int>(pbase) + r, H, D, h, d), v.x, v.y, v.z, v.w);
+      float4 v = *reinterpret_cast<const float4*>(obuf + r * OS + d);
+      const uint32_t off = part_off(static_cast<int>(pbase) + r, H, D, h, d);
+      if (fold) {
+        const float4 pv = ld_dev4(rs, off);
+        const float x = mbuf[r], y = nbuf[r];
+        v = make_float4(x * v.x + y * pv.x, x * v.y + y * pv.y, x * v.z + y * pv.z,
+                        x * v.w + y * pv.w);
+      }
+      st_dev4(rs, off, v.x, v.y, v.z, v.w);
     }
   }
   if (w == 0 && g == 0) {
@@ -1010,22 +1039,41 @@ __device__ __forceinline__ void kcf_f32_block(const KcfParams& P, int seg, int z
     if (g == 0) red[w][16 * t + l16] = ns;
   }
   __syncthreads();
+  // m_run is the same in every wavefront (block-wide maxima), so each lane
+  // derives its row's fold factors itself
+  const bool fold = sg.pad0 != 0;
 #pragma unroll
   for (int t = 0; t < NRT; ++t) {
     const int r = 16 * t + l16;
     if (r < nrows) {
       const size_t p = static_cast<size_t>(sg.part_base + (rb - sg.row_begin) + r);
       const __amdgpu_buffer_rsrc_t rs = part_rsrc(P.ws_o, P.o_bytes);
+      float* pml = reinterpret_cast<float*>(P.ws_ml + p * H + h);
+      float m = m_run[t], n = red[0][r] + red[1][r] + red[2][r] + red[3][r];
+      float x = 1.f, y = 0.f;
+      if (fold) {
+        // serial reduction: fold into the row's accumulator (Eqn 2)
+        const float mp = ld_dev(pml), np = ld_dev(pml + 1);
+        const float mx = fmaxf(m, mp);
+        x = fast_exp2(m - mx);
+        y = fast_exp2(mp - mx);
+        m = mx;
+        n = x * n + y * np;
+      }
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
-        const floatx4 v = acc[dt][t];
-        st_dev4(rs, part_off(static_cast<int>(p), H, D, h, w * (D / 4) + 16 * dt + 4 * g), v[0], v[1],
-                v[2], v[3]);
+        floatx4 v = acc[dt][t];
+        const uint32_t off = part_off(static_cast<int>(p), H, D, h, w * (D / 4) + 16 * dt + 4 * g);
+        if (fold) {
+          const float4 pv = ld_dev4(rs, off);
+          v = floatx4{x * v[0] + y * pv.x, x * v[1] + y * pv.y, x * v[2] + y * pv.z,
+                      x * v[3] + y * pv.w};
+        }
+        st_dev4(rs, off, v[0], v[1], v[2], v[3]);
       }
       if (w == 0 && g == 0) {
-        float* pml = reinterpret_cast<float*>(P.ws_ml + p * H + h);
-        st_dev(pml, m_run[t]);
-        st_dev(pml + 1, red[0][r] + red[1][r] + red[2][r] + red[3][r]);
+        st_dev(pml, m);
+        st_dev(pml + 1, n);
       }
     }
   }
@@ -1416,7 +1464,7 @@ __global__ __launch_bounds__(256) void ksf_kernel(KsfParams P) {
 
 template <typename T, int D, int NRT>
 hipError_t launch_phases(const TppParams& P, int n_sf, int schedule, int mask, hipStream_t s,
-                         const SideStream& side) {
+                         const SideStream& side, const int32_t* group_ptr, int n_groups) {
   const bool both = (mask & 3) == 3;
   if ((schedule == 1 || schedule == 2) && both) {
     // the fused launch always takes 16-row chunk-first blocks
@@ -1447,7 +1495,21 @@ hipError_t launch_phases(const TppParams& P, int n_sf, int schedule, int mask, h
     cf.cnt = nullptr;
     sf.cnt = nullptr;
   }
-  if ((mask & 1) && P.n_cf > 0) kcf_kernel<T, D, NRT><<<P.n_cf, 256, 0, s>>>(cf, P.zb);
+  if (schedule == 4) {
+    // serial reduction: the g-th launch runs every row's g-th chunk-first
+    // segment, which folds into the row's accumulator; the kernel boundary
+    // orders the writers of each row, so no row has two at once
+    if ((mask & 1) && P.n_cf > 0) {
+      for (int gi = 0; gi < n_groups; ++gi) {
+        KcfParams g = cf;
+        g.segs = cf.segs + group_ptr[gi];
+        const int nb = (group_ptr[gi + 1] - group_ptr[gi]) * P.zb * cf.H;
+        if (nb > 0) kcf_kernel<T, D, NRT><<<nb, 256, 0, s>>>(g, P.zb);
+      }
+    }
+  } else if ((mask & 1) && P.n_cf > 0) {
+    kcf_kernel<T, D, NRT><<<P.n_cf, 256, 0, s>>>(cf, P.zb);
+  }
   if ((mask & 2) && n_sf > 0) ksf_kernel<T, D><<<n_sf, 256, 0, s>>>(sf);
   return hipSuccess;
 }
@@ -1456,7 +1518,7 @@ template <typename T, int D>
 hipError_t launch_all(const AttnArgs& a, const DevWork& w, hipStream_t s, int mask,
                       const SideStream& side) {
   TppParams P;
-  const bool counting = w.schedule >= 2;  // the last contributor finishes each row
+  const bool counting = w.schedule == 2 || w.schedule == 3;  // the last contributor finishes each row
   P.cf = KcfParams{a.q, a.kpool, a.vpool, a.ss, a.hs, a.slot_len, w.segs, w.seg_slots, a.ws_o,
                    reinterpret_cast<float2*>(a.ws_ml), a.ws_o_bytes, a.H, a.C, a.qscale,
                    counting ? a.cnt : nullptr, a.o, w.part_ptr, w.parts};
@@ -1477,8 +1539,8 @@ hipError_t launch_all(const AttnArgs& a, const DevWork& w, hipStream_t s, int ma
   P.block_base = 0;
   const int n_sf = w.n_items * a.H;
   hipError_t e;
-  if (nrt == 1) e = launch_phases<T, D, 1>(P, n_sf, w.schedule, mask, s, side);
-  else e = launch_phases<T, D, 2>(P, n_sf, w.schedule, mask, s, side);
+  if (nrt == 1) e = launch_phases<T, D, 1>(P, n_sf, w.schedule, mask, s, side, w.seg_group_ptr, w.n_seg_groups);
+  else e = launch_phases<T, D, 2>(P, n_sf, w.schedule, mask, s, side, w.seg_group_ptr, w.n_seg_groups);
   if (e != hipSuccess) return e;
   // Partial-writing schedules finish their rows inside the kernels; the merge
   // epilogue runs in the sequential schedule (split rows) or on its own.

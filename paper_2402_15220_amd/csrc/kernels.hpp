@@ -24,7 +24,11 @@ struct DevWork {
   const int32_t* mg_rows = nullptr;
   int32_t n_mg = 0;
   int schedule = 0;  // 0 sequential, 1 fused + merge epilogue, 2 fused + in-kernel merge,
-                     // 3 concurrent streams + in-kernel merge
+                     // 3 concurrent streams + in-kernel merge, 4 serial reduction
+  // schedule 4: host array, segments [seg_group_ptr[g], seg_group_ptr[g+1])
+  // form the g-th chunk-first launch
+  const int32_t* seg_group_ptr = nullptr;
+  int32_t n_seg_groups = 0;
 };
 
 // Second stream and events for the concurrent schedule (default priority).

@@ -105,8 +105,16 @@ void build_tables(const ChunkTree& tree, Tables* out) {
 }
 
 void build_work(const ChunkTree& tree, const Tables& T, int32_t seg_chunks, int32_t split_chunks,
-                bool partial_items, int32_t num_heads, int32_t num_cus, WorkLists* out) {
+                bool partial_items, int32_t num_heads, int32_t num_cus, WorkLists* out,
+                bool serial_reduce) {
   WorkLists& W = *out;
+  if (serial_reduce) {
+    // every segment is one more launch: by default a run is one segment
+    // unless longer than 64 chunks
+    if (seg_chunks <= 0) seg_chunks = 64;
+    split_chunks = 0;
+    partial_items = false;
+  }
   const int64_t B = static_cast<int64_t>(T.row_seq.size());
   const size_t nn = T.node_slot.size();
 
@@ -211,6 +219,44 @@ void build_work(const ChunkTree& tree, const Tables& T, int32_t seg_chunks, int3
     return a.ce - a.cb > b.ce - b.cb;
   });
   W.n_parts = part;
+  W.seg_group_ptr.clear();
+  if (serial_reduce) {
+    // contributor position of each segment on its rows' paths: runs root ->
+    // leaf, segments in order (the same for every row a segment covers)
+    std::vector<int32_t> seg_k(W.segs.size(), -1);
+    for (int64_t r = 0; r < B; ++r) {
+      int32_t k = 0, last_run = -1;
+      for (int32_t e = T.path_ptr[r]; e < T.path_ptr[r + 1]; ++e) {
+        const int32_t ru = run_of[T.path_node[e]];
+        if (ru < 0 || ru == last_run) continue;
+        last_run = ru;
+        for (int32_t sgi = run_segs[ru].first; sgi < run_segs[ru].first + run_segs[ru].second; ++sgi)
+          seg_k[sgi] = k++;
+      }
+    }
+    // accumulator per row: partial index = row; rows with shared chunks fold it
+    W.parts.clear();
+    W.part_ptr.assign(1, 0);
+    for (int64_t r = 0; r < B; ++r) {
+      if (T.shr_ptr[r + 1] > T.shr_ptr[r]) W.parts.push_back(static_cast<int32_t>(r));
+      W.part_ptr.push_back(static_cast<int32_t>(W.parts.size()));
+    }
+    std::vector<int32_t> order(W.segs.size());
+    for (size_t i = 0; i < order.size(); ++i) order[i] = static_cast<int32_t>(i);
+    std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) { return seg_k[a] < seg_k[b]; });
+    std::vector<CfSeg> sorted;
+    for (int32_t i : order) {
+      CfSeg sg = W.segs[i];
+      sg.part_base = sg.row_begin;
+      sg.pad0 = seg_k[i] > 0 ? 1 : 0;
+      sorted.push_back(sg);
+      while (static_cast<int32_t>(W.seg_group_ptr.size()) <= seg_k[i])
+        W.seg_group_ptr.push_back(static_cast<int32_t>(sorted.size()) - 1);
+    }
+    W.seg_group_ptr.push_back(static_cast<int32_t>(sorted.size()));
+    W.segs.swap(sorted);
+    W.n_parts = B;
+  }
   W.row_of_seq.clear();
   for (int64_t r = 0; r < B; ++r) W.row_of_seq[T.row_seq[r]] = static_cast<int32_t>(r);
   W.item_of_row.assign(B, -1);

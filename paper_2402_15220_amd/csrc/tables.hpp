@@ -60,10 +60,20 @@ struct WorkLists {
   // `items` of each row's single item (-1: none or several pieces)
   std::unordered_map<int64_t, int32_t> row_of_seq;
   std::vector<int32_t> item_of_row;
+  // serial_reduce only: segments [seg_group_ptr[g], seg_group_ptr[g+1]) are
+  // the g-th contributors of their rows and run in the g-th launch
+  std::vector<int32_t> seg_group_ptr;
 };
 
+// serial_reduce: the partial-free variant (Section 3.3, further
+// optimizations): each row has one accumulator (partial index = row) that the
+// chunk-first segments fold into in path order, one launch per position in
+// that order (seg_group_ptr), so no row has two writers at once; segments
+// take up to 64 chunks (seg_chunks <= 0) and pad0 = 1 marks the ones that
+// fold (not the first on their rows' paths).
 void build_work(const ChunkTree& tree, const Tables& t, int32_t seg_chunks, int32_t split_chunks,
-                bool partial_items, int32_t num_heads, int32_t num_cus, WorkLists* out);
+                bool partial_items, int32_t num_heads, int32_t num_cus, WorkLists* out,
+                bool serial_reduce = false);
 
 // Bring work lists built for an earlier tree up to date when the only
 // structural changes since were new private chunks at the end of sequences'

@@ -1,6 +1,6 @@
 """The paper's microkernel experiments, re-run on one MI355X with synthetic data.
 
-    python -m paper_2402_15220_amd.sweeps [table3] [fig3] [fig4]
+    python -m paper_2402_15220_amd.sweeps [table3] [fig3] [fig4] [reduce]
 
 Workload of the experiments section (microkernel evaluation): batch mode, b
 sequences whose n_p prompt tokens start with n_s shared tokens, h=32 heads,
@@ -18,6 +18,13 @@ d=128, chunk c=64, fp16.
           attention) on the host clock.
   fig4    the same decode for n_c=64 tokens, n_s in 1024 and 2048, b from 16
           to 96 (Figure 4's batch sweep).
+  reduce  the two ways of reducing partials (Section 3.3, further
+          optimizations) on the static trees (one prompt of 1024 or 4096
+          tokens shared by 32 rows; a two-level tree of 64 rows): segmented
+          partials folded by the last contributor (schedule 2) or by the
+          sequence-first launch (schedule 0), against the partial-free
+          schedule 4 (one accumulator per row, folds serialised by launch
+          order). Workspace bytes and warm / cold time per call.
 
 Token ids follow the seeded recipe of ``workloads`` (uniform ids, distinct
 first unique tokens); K, V and q are N(0,1) fp16 draws of a seeded torch
@@ -200,6 +207,49 @@ def fig4(n_c=64):
             }), flush=True)
 
 
+def reduce_sweep(flush, warm_calls=100, cold_calls=20):
+    sys.path.insert(0, _root())
+    from workloads import make_static
+
+    for cfg in (2, 3, 4):
+        wl = make_static(cfg)
+        nodes = sum(-(-len(sg) // wl.c) for sg in wl.segments)
+        cache = Cache(wl.c, wl.H, wl.d, nodes + 16, dtype=torch.float16)
+        dev = [(torch.from_numpy(sg.k).cuda(), torch.from_numpy(sg.v).cuda()) for sg in wl.segments]
+        for sq in wl.seqs:
+            cache.insert(sq.seq_id, sq.tokens(wl.segments), torch.cat([dev[i][0] for i in sq.segs]),
+                         torch.cat([dev[i][1] for i in sq.segs]))
+        del dev
+        rows = cache.seq_order()
+        q = torch.from_numpy(np.ascontiguousarray(wl.q[rows])).cuda()
+        o = torch.empty_like(q)
+        model = call_model(cache.tables(), wl.H, wl.d, 2)
+
+        def call():
+            cache.attention(q, out=o)
+
+        first = None
+        for sched, seg in ((2, -1), (0, -1), (4, -1), (4, 4)):
+            cache.set_tuning(seg_chunks=seg, split_chunks=0, phase_mask=7, schedule=sched)
+            call()
+            torch.cuda.synchronize()
+            if first is None:
+                first = o.float().clone()
+            diff = float((o.float() - first).abs().max())
+            warm = _events_mean(call, warm_calls)
+            cold = _cold_median(call, flush, cold_calls)
+            print(json.dumps({
+                "sweep": "reduce", "config": cfg, "rows": int(len(rows)), "schedule": sched,
+                "seg_chunks": cache.stats()["seg_chunks"], "workspace_bytes": cache.workspace()[1],
+                "us_warm": round(warm, 2), "us_cold": round(cold, 2),
+                "hbm_frac_warm": round(model["total"] / (warm * 1e-6) / 1e9 / PEAK_HBM_GBPS, 4),
+                "max_diff_vs_schedule_2": diff,
+            }), flush=True)
+        cache.close()
+        del cache, q, o
+        torch.cuda.empty_cache()
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("which", nargs="*", default=["table3", "fig3", "fig4"])
@@ -207,7 +257,8 @@ def main(argv=None):
     torch.cuda.set_device(0)
     flush = torch.ones(1 << 29, dtype=torch.float16, device="cuda")  # 1 GiB
     for w in args.which:
-        {"table3": lambda: table3(flush), "fig3": fig3, "fig4": fig4}[w]()
+        {"table3": lambda: table3(flush), "fig3": fig3, "fig4": fig4,
+         "reduce": lambda: reduce_sweep(flush)}[w]()
 
 
 if __name__ == "__main__":

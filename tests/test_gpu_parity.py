@@ -51,7 +51,8 @@ def test_static_config(cfg, layout):
 
 @pytest.mark.parametrize("seg,split,sched", [(1, 0, 0), (16, 0, 0), (4, 3, 0), (2, 1, 0), (64, 5, 0),
                                              (1, 0, 1), (4, 0, 1), (16, 3, 1), (3, 1, 1),
-                                             (1, 0, 2), (8, 0, 2), (16, 2, 2), (64, 1, 2), (4, 0, 3), (16, 3, 3)])
+                                             (1, 0, 2), (8, 0, 2), (16, 2, 2), (64, 1, 2), (4, 0, 3), (16, 3, 3),
+                                             (-1, 0, 4), (1, 0, 4), (5, 3, 4)])
 def test_config2_work_partitions(seg, split, sched):
     """Every schedule, segment size and split gives the same result, and
     repeated calls (counters reset by the kernels) stay correct."""
@@ -63,6 +64,21 @@ def test_config2_work_partitions(seg, split, sched):
         o, q, row_seq = p.attention({s.seq_id: wl.q[s.seq_id] for s in wl.seqs})
         ref = p.reference(row_seq, q, 0.0) if rep == 0 else ref
         assert_close(o, ref, wl.dtype, f"config 2 seg={seg} split={split} schedule={sched} rep={rep}")
+
+
+@pytest.mark.parametrize("cfg,seg", [(3, -1), (4, -1), (4, 1)])
+def test_partial_free_multi_level(cfg, seg):
+    """The partial-free schedule on trees with several levels of sharing:
+    rows fold segments of different levels into one accumulator, one launch
+    per position along the path."""
+    print(f"[case] static config {cfg} schedule 4 seg={seg}", flush=True)
+    wl = make_static(cfg)
+    p = _static_pair(wl)
+    p.cache.set_tuning(seg_chunks=seg, schedule=4)
+    for rep in range(2):
+        o, q, row_seq = p.attention({s.seq_id: wl.q[s.seq_id] for s in wl.seqs})
+        ref = p.reference(row_seq, q, 0.0) if rep == 0 else ref
+        assert_close(o, ref, wl.dtype, f"config {cfg} schedule 4 seg={seg} rep={rep}")
 
 
 @pytest.mark.timeout(900)
@@ -121,6 +137,8 @@ def test_random_trees(seed):
     H = 1 + seed % 3
     print(f"[case] random tree seed={seed} c={c} d={d} H={H} dtype={np.dtype(dtype).name}", flush=True)
     p = Pair(c, H, d, dtype, 4096, layout="interleaved" if seed % 5 == 2 else "split")
+    if seed % 3 == 1:  # the partial-free schedule, one segment per chunk or per run
+        p.cache.set_tuning(seg_chunks=1 if seed % 2 else -1, schedule=4)
     full = {}
     qrng = np.random.default_rng(1000 + seed)
     ops = random_op_script(seed, n_ops=50, alphabet=3, max_len=max(12, 2 * c + 3))

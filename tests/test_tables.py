@@ -266,10 +266,13 @@ def test_decode_growth_updates_context_in_place():
 @pytest.mark.parametrize("seed", range(12))
 def test_random_growth_patches_match_rebuild(seed):
     """Small trees, small chunks: appends and extends that grow private chains,
-    mixed with inserts, splits and removals (which rebuild)."""
+    mixed with inserts, splits and removals (which rebuild). Every third seed
+    runs the partial-free schedule's work lists."""
     _lib_or_skip()
     c = 1 + seed % 4
     h = _checked_cache(c, 1, 64, B.CA_FP16, 1 << 20)
+    if seed % 3 == 2:
+        B.ca_set_tuning(h, schedule=4)
     live = set()
     for op in random_op_script(seed, n_ops=120, alphabet=3, max_len=2 * c + 3):
         if op[0] in ("extend", "remove") and op[1] not in live:
@@ -289,4 +292,34 @@ def test_random_growth_patches_match_rebuild(seed):
             live.discard(op[1])
         B.ca_seq_order(h)
         B.ca_stats(h)
+    B.ca_destroy(h)
+
+
+def _align(x, a=256):
+    return (x + a - 1) // a * a
+
+
+def test_partial_free_workspace_is_one_accumulator_per_row():
+    """Section 3.3 (further optimizations): the partial-free schedule keeps one
+    (O, m, n) per (sequence, head), however many shared segments and tree
+    levels a row's path crosses; the partial-writing schedules keep one per
+    (segment, row, head) plus one per split or partial-writing item."""
+    _lib_or_skip()
+    H, d = 2, 64
+    h = B.ca_create(2, H, d, B.CA_FP16, 256)
+    # three levels of sharing: [1..8] by all, [9, 10] by 0-2, [11, 12] by 0-1
+    for sid, tail in enumerate([[9, 10, 11, 12, 20], [9, 10, 11, 12, 21], [9, 10, 22], [23]]):
+        B.ca_insert(h, sid, list(range(1, 9)) + tail)
+    Bn = 4
+    B.ca_set_tuning(h, seg_chunks=1, schedule=2)
+    ws2 = B.ca_workspace_size(h)
+    B.ca_set_tuning(h, schedule=4)
+    ws4 = B.ca_workspace_size(h)
+    assert ws4 == _align(Bn * H * d * 4) + _align(Bn * H * 2 * 4)
+    # 4 + 1 + 1 single-chunk segments over 4, 3, 2 rows, plus 4 own items
+    n2 = 4 * 4 + 1 * 3 + 1 * 2 + 4
+    assert ws2 == _align(n2 * H * d * 4) + _align(n2 * H * 2 * 4)
+    B.ca_set_tuning(h, seg_chunks=-1)   # automatic: one segment per run
+    assert B.ca_stats(h)["seg_chunks"] == 64
+    assert B.ca_workspace_size(h) == ws4
     B.ca_destroy(h)
