@@ -106,11 +106,14 @@ def main():
 
     def back_to_back(fn, n):
         """Mean device time per fn() over n back-to-back launches, with events
-        on the launch stream (no host synchronisation in between)."""
+        on the launch stream (no host synchronisation in between). A spin
+        kernel holds the stream while the host enqueues, so a launch that is
+        shorter than the host's per-call cost still runs back to back."""
         fn()
         torch.cuda.synchronize()
         a = torch.cuda.Event(enable_timing=True)
         b = torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(40_000_000)
         a.record()
         for _ in range(n):
             fn()
