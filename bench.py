@@ -302,7 +302,9 @@ def dynamic_run():
     steps are generated and copied to the GPU first; each step then times the
     library calls only: attention alone with events, and the whole step
     (remove/insert, append, row order, q permutation, attention) on the host
-    clock up to a synchronisation."""
+    clock up to a synchronisation. A first, pipelined pass runs the same
+    steps with no synchronisation in between and reports wall time per step
+    against the GPU's busy span (host work hidden under device work)."""
     import numpy as np
     import torch
 
@@ -339,16 +341,13 @@ def dynamic_run():
                           torch.from_numpy(st.q).cuda()))
     q_rows = torch.empty((256, wl.H, wl.d), dtype=torch.float16, device="cuda")
     o = torch.empty_like(q_rows)
+    pinned_idx = torch.empty((len(dev_steps), 256), dtype=torch.int64, pin_memory=True)
     torch.cuda.synchronize()
     t_gen = time.perf_counter() - t_gen
     st0 = cache.stats()
     up0, pa0 = st0["uploads"], st0["patches"]
 
-    att_us, step_us, rows = [], [], []
-    for st, added, k, v, q in dev_steps:
-        a = torch.cuda.Event(enable_timing=True)
-        b = torch.cuda.Event(enable_timing=True)
-        t0 = time.perf_counter()
+    def one_step(i, st, added, k, v, q):
         if st.churn:
             for sid in st.churn.removed:
                 cache.remove(sid)
@@ -356,10 +355,55 @@ def dynamic_run():
                 cache.insert(sid, toks, kk, vv)
         cache.append(st.live, st.tokens, k, v)
         order = cache.seq_order()
-        pos = np.searchsorted(st.live, order)
         n = len(order)
-        idx = torch.from_numpy(pos).cuda(non_blocking=True)
+        pinned_idx[i, :n] = torch.from_numpy(np.searchsorted(st.live, order))
+        idx = pinned_idx[i, :n].cuda(non_blocking=True)
         torch.index_select(q, 0, idx, out=q_rows[:n])
+        return n
+
+    # Pipelined pass: no synchronisation between steps, so the host work of a
+    # step (tree update, context patch or rebuild and upload, launches) runs
+    # while the GPU still executes earlier steps (latency hiding). Runs on a
+    # copy of the starting tree and leaves it as the timed pass expects.
+    pipe = {}
+    if len(dev_steps) > 0:
+        # one call on the starting tree first: the library's one-time device
+        # and pinned allocations stay out of the pipelined span
+        q_rows.zero_()
+        n0 = len(cache.seq_order())
+        cache.attention(q_rows[:n0], out=o[:n0])
+        ga = torch.cuda.Event(enable_timing=True)
+        gb = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        ga.record()
+        for i, (st, added, k, v, q) in enumerate(dev_steps):
+            n = one_step(i, st, added, k, v, q)
+            cache.attention(q_rows[:n], out=o[:n])
+        gb.record()
+        host_done = time.perf_counter()
+        gb.synchronize()
+        wall = time.perf_counter() - t0
+        pipe = {"step_us_pipelined": wall * 1e6 / len(dev_steps),
+                "host_enqueue_us_per_step": (host_done - t0) * 1e6 / len(dev_steps),
+                "gpu_us_per_step_pipelined": ga.elapsed_time(gb) * 1e3 / len(dev_steps)}
+        # back to the starting tree for the per-step timed pass
+        for sid in list(cache.seq_order()):
+            cache.remove(int(sid))
+        for s in wl.seqs:
+            k, v = full_kv(s)
+            cache.insert(s.seq_id, s.tokens(wl.segments), k, v)
+            del k, v
+        torch.cuda.synchronize()
+        st0 = cache.stats()
+        up0, pa0 = st0["uploads"], st0["patches"]
+
+    att_us, step_us, rows = [], [], []
+    for i, (st, added, k, v, q) in enumerate(dev_steps):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        t0 = time.perf_counter()
+        n = one_step(i, st, added, k, v, q)
         a.record()
         cache.attention(q_rows[:n], out=o[:n])
         b.record()
@@ -376,7 +420,8 @@ def dynamic_run():
             "attention_us_mean": float(np.mean(att_us)), "attention_us_median": float(np.median(att_us)),
             "step_us_mean": float(np.mean(step_us)), "step_us_median": float(np.median(step_us)),
             "tok_per_s": float(sum(rows) / (sum(att_us) * 1e-6)),
-            "context_uploads": int(up), "context_patched_in_place": int(pa), "setup_s": t_gen}
+            "context_uploads": int(up), "context_patched_in_place": int(pa), "setup_s": t_gen,
+            **pipe}
 
 
 def cpu_baseline(wl, rows, seconds):
