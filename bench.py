@@ -246,7 +246,8 @@ def cold_times(call, cache, model, n=30):
 def prefill_run(n=100):
     """Prefill with prefix reuse: the joining sequence's 512 new tokens attend
     causally over its 1536 positions (1024 reused from the tree). Event-timed
-    back-to-back calls on the launch stream."""
+    back-to-back calls on the launch stream, enqueued behind a spin kernel so
+    the host's per-call cost stays out of the figure."""
     import numpy as np
     import torch
 
@@ -273,6 +274,7 @@ def prefill_run(n=100):
     torch.cuda.synchronize()
     a = torch.cuda.Event(enable_timing=True)
     b = torch.cuda.Event(enable_timing=True)
+    torch.cuda._sleep(40_000_000)   # hold the stream while the calls are enqueued
     a.record()
     for _ in range(n):
         call()

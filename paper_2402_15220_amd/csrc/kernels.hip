@@ -1087,13 +1087,15 @@ __device__ __forceinline__ void kcf_f32_block(const KcfParams& P, int seg, int z
 // chunk along the root-to-leaf path. Query i sits at position
 // L - n_q + i and sees positions 0..L - n_q + i.
 //
-// One block per (64 queries, head), NGRP groups of four wavefronts. Group
+// One block per (64 queries, head), NGRP groups of WPG wavefronts. Group
 // k takes chunks k, k+NGRP, ... of the path, so NGRP chunks are in flight
-// per block; inside a group, wavefront w owns queries [16w, 16w+16) of the
-// tile and every token of the group's chunks. Per chunk (up to 64 tokens),
-// the group stages K and V as [token][d] in its LDS tile, once for all 64
+// per block; inside a group, wavefront w owns QT = 4/WPG tiles of 16 queries
+// and every token of the group's chunks. Per chunk (up to 64 tokens), the
+// group stages K and V as [token][d] in its LDS tile, once for all 64
 // queries; the group's next chunk is already loading into registers while
-// the current one is used.
+// the current one is used. Each K or V element read from LDS feeds QT
+// matrix-core ops, so more queries per wavefront mean less LDS traffic per
+// FLOP (the tile reads, not the MFMAs, bound this kernel).
 //   S^T = K Q^T  (16x16x32 MFMA: K rows from LDS as A, the wavefront's q rows
 //                 as B, held in registers for the whole call);
 //   causal and chunk-length mask, online softmax per query row (base 2);
@@ -1120,23 +1122,19 @@ struct KpfParams {
 template <int D>
 constexpr int kpf_k_stride() { return D + 8; }   // halves per K (and V) row in LDS
 
-// K granule e = tid + 256u: token e / NG, column e % NG (coalesced rows).
-// V granule: token tid % 64, column tid / 64 + 4u (a wavefront covers all 64
-// tokens of one column, so the transposed LDS writes are contiguous). Rows
-// past the chunk's length re-read its last row (their scores are masked).
-// One chunk's K and V rows for the group's 256 threads: granule e = tid +
-// 256u is token e / (D/8), 16-byte column e % (D/8) (coalesced rows). Rows
-// past the chunk's length re-read its last row (their scores are masked).
-template <int D>
+// One chunk's K and V rows for a group of GT threads: granule e = tid + GT*u
+// is token e / (D/8), 16-byte column e % (D/8) (coalesced rows). Rows past
+// the chunk's length re-read its last row (their scores are masked).
+template <int D, int GT>
 __device__ __forceinline__ void kpf_load_chunk(const _Float16* kbase, const _Float16* vbase,
                                                size_t slot_stride, int slot, int len, int tid,
-                                               u32x4 (&kr)[D / 32], u32x4 (&vr)[D / 32]) {
+                                               u32x4 (&kr)[D * 8 / GT], u32x4 (&vr)[D * 8 / GT]) {
   constexpr int NG = D / 8;
   const _Float16* kb = kbase + slot * slot_stride;
   const _Float16* vb = vbase + slot * slot_stride;
 #pragma unroll
-  for (int u = 0; u < D / 32; ++u) {
-    const int e = tid + 256 * u;
+  for (int u = 0; u < D * 8 / GT; ++u) {
+    const int e = tid + GT * u;
     const size_t off = static_cast<size_t>(min(e / NG, len - 1)) * D + (e % NG) * 8;
     kr[u] = *reinterpret_cast<const u32x4*>(kb + off);
     vr[u] = *reinterpret_cast<const u32x4*>(vb + off);
@@ -1146,52 +1144,77 @@ __device__ __forceinline__ void kpf_load_chunk(const _Float16* kbase, const _Flo
 template <int D>
 constexpr int kpf_tile_bytes() { return 2 * 64 * kpf_k_stride<D>() * 2; }
 
-template <int D, int NGRP>
-__global__ __launch_bounds__(256 * NGRP) void kpf_kernel(KpfParams P,
-                                                          const int32_t* __restrict__ chunk_slot,
-                                                          const int32_t* __restrict__ chunk_start) {
+template <int D, int NGRP, int WPG>
+__global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
+                                                              const int32_t* __restrict__ chunk_slot,
+                                                              const int32_t* __restrict__ chunk_start) {
+  constexpr int QT = 4 / WPG;       // 16-query tiles per wavefront
+  constexpr int GT = 64 * WPG;      // threads per group
   constexpr int KS = D / 32;        // 16x16x32 steps over d
   constexpr int DT = D / 16;        // 16-wide d tiles of O^T
   constexpr int NG = D / 8;         // 16-byte granules per token row
-  constexpr int GPT = NG / 4;       // granules of K (and of V) per thread per chunk
+  constexpr int GPT = 64 * NG / GT; // granules of K (and of V) per thread per chunk
   constexpr int KST = kpf_k_stride<D>();
   constexpr int TB = kpf_tile_bytes<D>();
-  static_assert(NGRP == 1 || TB * NGRP >= (NGRP - 1) * 64 * (D + 2) * 4, "merge buffer");
-  __shared__ __attribute__((aligned(16))) char lds[TB * NGRP];
+  constexpr int OST = D + 4;         // merge buffer row stride (floats): rows start 4 banks apart
+  static_assert(WPG * QT == 4, "64 queries per block");
+  static_assert(2 * TB * NGRP <= 160 * 1024, "two LDS tiles per group");
+  static_assert(NGRP == 1 || 2 * TB * NGRP >= (NGRP - 1) * 64 * (OST + 2) * 4, "merge buffer");
+  __shared__ __attribute__((aligned(16))) char lds[2 * TB * NGRP];
 
-  const int tid = threadIdx.x, lane = tid & 63, w = (tid >> 6) & 3;
-  const int grp = __builtin_amdgcn_readfirstlane(tid >> 8);  // uniform: chunk indices stay scalar
-  const int gtid = tid & 255;  // thread index inside the group
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int grp = __builtin_amdgcn_readfirstlane((tid >> 6) / WPG);  // uniform: chunk indices stay scalar
+  const int w = (tid >> 6) % WPG;   // wavefront inside the group
+  const int gtid = tid % GT;        // thread index inside the group
   const int l16 = lane & 15, g = lane >> 4;
-  _Float16* k_lds = reinterpret_cast<_Float16*>(lds + grp * TB);
-  _Float16* v_lds = k_lds + 64 * KST;
-  const int h = blockIdx.y;
-  const int H = P.H, C = P.C, n_q = P.n_q;
+  // the group's two tiles: tile b holds K rows then V rows
+  auto tile_k = [&](int b) { return reinterpret_cast<_Float16*>(lds + (2 * grp + b) * TB); };
+  // XCD-aware tile order: blocks go to the eight XCDs round-robin, so block
+  // b runs on XCD b % 8; the tiles (head-major) are split into eight
+  // contiguous ranges, one per XCD, and every query tile of a head reads
+  // that head's chunks through the same L2.
+  const int H = P.H, n_q = P.n_q;
+  const int n_qt = (n_q + 63) / 64;
+  const int per_xcd = static_cast<int>(gridDim.x) / 8;
+  const int v = static_cast<int>(blockIdx.x % 8) * per_xcd + static_cast<int>(blockIdx.x / 8);
+  if (v >= n_qt * H) return;
+  const int h = v / n_qt;
   const int L = chunk_start[P.n_chunks];
-  const int q0 = static_cast<int>(blockIdx.x) * 64;           // first query of the tile
-  const int qi = q0 + 16 * w + l16;                            // this lane's query row
-  const int pos = L - n_q + qi;                                // its position
+  const int q0 = (v % n_qt) * 64;                              // first query of the tile
   const int pos_last = L - n_q + min(q0 + 63, n_q - 1);        // last position of the tile
+  const int pos_first = L - n_q + q0;                          // first position of the tile
   const size_t slot_stride = static_cast<size_t>(P.ss);
   const _Float16* kbase = P.kpool + h * P.hs;
   const _Float16* vbase = P.vpool + h * P.hs;
 
-  half8 qf[KS];
+  // this lane's query row of tile t, and its position
+  int qi[QT], pos[QT];
+  half8 qf[QT][KS];
 #pragma unroll
-  for (int s = 0; s < KS; ++s) {
-    if (qi < n_q)
-      qf[s] = *reinterpret_cast<const half8*>(P.q + (static_cast<size_t>(qi) * H + h) * D + 32 * s +
-                                              8 * g);
-    else
-      qf[s] = half8{};
+  for (int t = 0; t < QT; ++t) {
+    qi[t] = q0 + 16 * (QT * w + t) + l16;
+    pos[t] = L - n_q + qi[t];
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      if (qi[t] < n_q)
+        qf[t][s] = *reinterpret_cast<const half8*>(P.q + (static_cast<size_t>(qi[t]) * H + h) * D +
+                                                   32 * s + 8 * g);
+      else
+        qf[t][s] = half8{};
+    }
   }
   // q has arrived before any chunk load is issued, so the MFMAs inside the
   // loop never wait on vector memory (the next chunk's loads stay in flight)
   wait_stores();
-  float m_run = kNegBig, n_part = 0.f;
-  floatx4 acc[DT];
+  float m_run[QT], n_part[QT];
+  floatx4 acc[QT][DT];
 #pragma unroll
-  for (int dt = 0; dt < DT; ++dt) acc[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+  for (int t = 0; t < QT; ++t) {
+    m_run[t] = kNegBig;
+    n_part[t] = 0.f;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) acc[t][dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+  }
 
   // Chunks the tile needs: those starting at or before its last position
   // (starts ascend); 64 starts per load, one per lane.
@@ -1205,151 +1228,197 @@ __global__ __launch_bounds__(256 * NGRP) void kpf_kernel(KpfParams P,
   }
   // Per-chunk metadata comes through the scalar cache (uniform index,
   // read-only arguments), so no metadata load ever waits behind the chunk
-  // rows in flight. Two register buffers per group: chunk j's rows arrive
-  // while chunk j - NGRP is used, and chunk j + NGRP's loads are issued
-  // before chunk j is used, so two chunks per group are in flight.
-  auto issue = [&](u32x4 (&kr)[GPT], u32x4 (&vr)[GPT], int j) {
+  // rows in flight. Past the end the registers reload the group's last
+  // chunk: every step issues the same loads, so the wait before each LDS
+  // write covers exactly the registers it needs on every path.
+  u32x4 kr[GPT], vr[GPT];
+  auto issue = [&](int j) {
+    j = min(j, n_ch - 1);
     const int st = chunk_start[j];
-    kpf_load_chunk<D>(kbase, vbase, slot_stride, chunk_slot[j], chunk_start[j + 1] - st, gtid, kr,
-                      vr);
+    kpf_load_chunk<D, GT>(kbase, vbase, slot_stride, chunk_slot[j], chunk_start[j + 1] - st, gtid,
+                          kr, vr);
   };
-  auto step = [&](u32x4 (&kr)[GPT], u32x4 (&vr)[GPT], int j) {
-    const bool have = j < n_ch;
-    __syncthreads();  // every wavefront is done with the previous chunk's LDS
-    if (have) {
+  auto stage = [&](int b) {
+    _Float16* k_lds = tile_k(b);
+    _Float16* v_lds = k_lds + 64 * KST;
 #pragma unroll
-      for (int u = 0; u < GPT; ++u) {
-        const int e = gtid + 256 * u;
-        *reinterpret_cast<u32x4*>(k_lds + (e / NG) * KST + (e % NG) * 8) = kr[u];
-        *reinterpret_cast<u32x4*>(v_lds + (e / NG) * KST + (e % NG) * 8) = vr[u];
-      }
+    for (int u = 0; u < GPT; ++u) {
+      const int e = gtid + GT * u;
+      *reinterpret_cast<u32x4*>(k_lds + (e / NG) * KST + (e % NG) * 8) = kr[u];
+      *reinterpret_cast<u32x4*>(v_lds + (e / NG) * KST + (e % NG) * 8) = vr[u];
     }
-    // The chunk these registers load next. Past the end they reload the last
-    // chunk: every step issues the same loads, so the wait before each LDS
-    // write covers exactly the registers it needs on every path.
-    const int jn = min(j + 2 * NGRP, n_ch - 1);
-    __syncthreads();
-    issue(kr, vr, jn);  // in flight while this chunk and the next are used
-    if (!have) return;
+  };
+  auto compute = [&](int j, int b) {
+    const _Float16* k_lds = tile_k(b);
+    const _Float16* v_lds = k_lds + 64 * KST;
     const int c0 = chunk_start[j];
     const int len = chunk_start[j + 1] - c0;
 
-    // S^T for the chunk's 64 token slots: tile jt holds tokens 16jt..16jt+15
-    floatx4 sacc[4];
+    // S^T for the chunk's 64 token slots: tile jt holds tokens 16jt..16jt+15;
+    // each K read feeds the wavefront's QT query tiles
+    floatx4 sacc[QT][4];
 #pragma unroll
     for (int jt = 0; jt < 4; ++jt) {
-      sacc[jt] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int t = 0; t < QT; ++t) sacc[t][jt] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int s = 0; s < KS; ++s) {
         const half8 ka = *reinterpret_cast<const half8*>(k_lds + (16 * jt + l16) * KST + 32 * s + 8 * g);
-        sacc[jt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ka, qf[s], sacc[jt], 0, 0, 0);
+#pragma unroll
+        for (int t = 0; t < QT; ++t)
+          sacc[t][jt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ka, qf[t][s], sacc[t][jt], 0, 0, 0);
       }
     }
-    // lane holds S^T[token 16jt + 4g + i][row l16]
-    float lmax = kNegBig;
+    // lane holds S^T[token 16jt + 4g + i][row l16 of tile t] (unscaled).
+    // Chunks that are whole and end before the tile's first position need
+    // no mask (uniform test).
+    if (len < 64 || c0 + 63 > pos_first) {
 #pragma unroll
-    for (int jt = 0; jt < 4; ++jt) {
+      for (int t = 0; t < QT; ++t)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int t = 16 * jt + 4 * g + i;
-        const float x = (t < len && c0 + t <= pos) ? sacc[jt][i] * P.qscale : -INFINITY;
-        sacc[jt][i] = x;
-        lmax = fmaxf(lmax, x);
-      }
+        for (int jt = 0; jt < 4; ++jt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int tk = 16 * jt + 4 * g + i;
+            if (!(tk < len && c0 + tk <= pos[t])) sacc[t][jt][i] = -INFINITY;
+          }
     }
-    lmax = fmaxf(lmax, __shfl_xor(lmax, 16));
-    lmax = fmaxf(lmax, __shfl_xor(lmax, 32));
-    const float mn = fmaxf(m_run, lmax);
-    const float alpha = fast_exp2(m_run - mn);
-    m_run = mn;
-    half4 ph[4];
-    float ps = 0.f;
+    half8 pb[QT][2];
+    bool moved = false;
+    float alpha[QT];
 #pragma unroll
-    for (int jt = 0; jt < 4; ++jt) {
+    for (int t = 0; t < QT; ++t) {
+      float lmax = -INFINITY;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        ph[jt][i] = static_cast<_Float16>(fast_exp2(sacc[jt][i] - mn));
-        ps += static_cast<float>(ph[jt][i]);
+      for (int jt = 0; jt < 4; ++jt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) lmax = fmaxf(lmax, sacc[t][jt][i]);
+      lmax = fmaxf(lmax, __shfl_xor(lmax, 16));
+      lmax = fmaxf(lmax, __shfl_xor(lmax, 32));
+      // running max in scaled base-2 units; qscale > 0 commutes with max
+      const float mn = fmaxf(m_run[t], lmax * P.qscale);
+      alpha[t] = fast_exp2(m_run[t] - mn);
+      moved |= alpha[t] != 1.f;
+      m_run[t] = mn;
+      half4 ph[4];
+      float ps = 0.f;
+#pragma unroll
+      for (int jt = 0; jt < 4; ++jt) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float pv = fast_exp2(__builtin_fmaf(sacc[t][jt][i], P.qscale, -mn));
+          ph[jt][i] = static_cast<_Float16>(pv);
+          ps += pv;
+        }
       }
-    }
-    n_part = n_part * alpha + ps;
-    // O^T += V^T P^T over 32 tokens per 16x16x32 MFMA: lane group g's
-    // 8-token K-slice is tokens 4g..4g+3 of tiles 2p and 2p+1 (any token
-    // order works as long as both operands share it), which is exactly what
-    // the lane holds of P^T, and two transposing reads fetch the V^T side.
-    half8 pb[2];
+      n_part[t] = n_part[t] * alpha[t] + ps;
+      // O^T += V^T P^T over 32 tokens per 16x16x32 MFMA: lane group g's
+      // 8-token K-slice is tokens 4g..4g+3 of token tiles 2p and 2p+1 (any
+      // token order works as long as both operands share it), which is
+      // exactly what the lane holds of P^T; two transposing reads fetch the
+      // V^T side.
 #pragma unroll
-    for (int p2 = 0; p2 < 2; ++p2)
-      pb[p2] = __builtin_shufflevector(ph[2 * p2], ph[2 * p2 + 1], 0, 1, 2, 3, 4, 5, 6, 7);
+      for (int p2 = 0; p2 < 2; ++p2)
+        pb[t][p2] = __builtin_shufflevector(ph[2 * p2], ph[2 * p2 + 1], 0, 1, 2, 3, 4, 5, 6, 7);
+    }
+    // O is rescaled only when some row's maximum moved (uniform test)
+    if (__any(moved)) {
+#pragma unroll
+      for (int t = 0; t < QT; ++t)
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) acc[t][dt] *= alpha[t];
+    }
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
-      acc[dt] *= alpha;
 #pragma unroll
       for (int p2 = 0; p2 < 2; ++p2) {
         const _Float16* vp = v_lds + (32 * p2 + 4 * g + (l16 >> 2)) * KST + 16 * dt + 4 * (l16 & 3);
         const half4 v0 = lds_read_tr16(vp);             // tokens 32p + 4g + j
         const half4 v1 = lds_read_tr16(vp + 16 * KST);  // tokens 32p + 16 + 4g + j
         const half8 va = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
-        acc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(va, pb[p2], acc[dt], 0, 0, 0);
+#pragma unroll
+        for (int t = 0; t < QT; ++t)
+          acc[t][dt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(va, pb[t][p2], acc[t][dt], 0, 0, 0);
       }
     }
   };
-  u32x4 kr0[GPT], vr0[GPT], kr1[GPT], vr1[GPT];
-  if (n_ch > 0) {
-    issue(kr0, vr0, min(grp, n_ch - 1));
-    issue(kr1, vr1, min(grp + NGRP, n_ch - 1));
+  // Two LDS tiles per group: step i computes the group's chunk i from tile
+  // i % 2 while chunk i + 1 is written into the other tile and chunk i + 2
+  // loads into the registers; one barrier per step (after it, tile i % 2 is
+  // complete and nobody still reads the other one).
+  const int steps = (n_ch + NGRP - 1) / NGRP;  // the same in every group
+  if (steps > 0) {
+    issue(grp);
+    stage(0);
+    issue(grp + NGRP);
   }
-  // the same even number of steps in every group (steps past the end only
-  // keep the barriers and the load pattern)
-  const int steps = 2 * ((n_ch + 2 * NGRP - 1) / (2 * NGRP));
-  for (int i = 0; i < steps; i += 2) {
-    step(kr0, vr0, grp + i * NGRP);
-    step(kr1, vr1, grp + (i + 1) * NGRP);
+  for (int i = 0; i < steps; ++i) {
+    __syncthreads();
+    if (i + 1 < steps) {
+      stage((i + 1) & 1);
+      issue(grp + (i + 2) * NGRP);
+    }
+    const int j = grp + i * NGRP;
+    if (j < n_ch) compute(j, i & 1);
   }
   // row sums over the four lane groups
-  float n_row = n_part;
-  n_row += __shfl_xor(n_row, 16);
-  n_row += __shfl_xor(n_row, 32);
+  float n_row[QT];
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    n_row[t] = n_part[t];
+    n_row[t] += __shfl_xor(n_row[t], 16);
+    n_row[t] += __shfl_xor(n_row[t], 32);
+  }
   if constexpr (NGRP > 1) {
     // groups 1.. hand their (m, n, O) to group 0 through LDS (Eqn 2)
-    float* ob = reinterpret_cast<float*>(lds);                    // [NGRP-1][64][D]
-    float* mb = ob + (NGRP - 1) * 64 * D;                          // [NGRP-1][64][2]
-    const int r = 16 * w + l16;
+    float* ob = reinterpret_cast<float*>(lds);                    // [NGRP-1][64][OST]
+    float* mb = ob + (NGRP - 1) * 64 * OST;                        // [NGRP-1][64][2]
     __syncthreads();  // the tiles are free
     if (grp > 0) {
-      float* o_ = ob + ((grp - 1) * 64 + r) * D;
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
-        *reinterpret_cast<floatx4*>(o_ + 16 * dt + 4 * g) = acc[dt];
-      if (g == 0) {
-        mb[((grp - 1) * 64 + r) * 2] = m_run;
-        mb[((grp - 1) * 64 + r) * 2 + 1] = n_row;
+      for (int t = 0; t < QT; ++t) {
+        const int r = 16 * (QT * w + t) + l16;
+        float* o_ = ob + ((grp - 1) * 64 + r) * OST;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+          *reinterpret_cast<floatx4*>(o_ + 16 * dt + 4 * g) = acc[t][dt];
+        if (g == 0) {
+          mb[((grp - 1) * 64 + r) * 2] = m_run[t];
+          mb[((grp - 1) * 64 + r) * 2 + 1] = n_row[t];
+        }
       }
     }
     __syncthreads();
     if (grp > 0) return;
 #pragma unroll
-    for (int k = 1; k < NGRP; ++k) {
-      const float mo = mb[((k - 1) * 64 + r) * 2], no = mb[((k - 1) * 64 + r) * 2 + 1];
-      const float M = fmaxf(m_run, mo);
-      const float ws = fast_exp2(m_run - M), wo = fast_exp2(mo - M);
-      const float* o_ = ob + ((k - 1) * 64 + r) * D;
+    for (int t = 0; t < QT; ++t) {
+      const int r = 16 * (QT * w + t) + l16;
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
-        acc[dt] = acc[dt] * ws + *reinterpret_cast<const floatx4*>(o_ + 16 * dt + 4 * g) * wo;
-      n_row = n_row * ws + no * wo;
-      m_run = M;
+      for (int k = 1; k < NGRP; ++k) {
+        const float mo = mb[((k - 1) * 64 + r) * 2], no = mb[((k - 1) * 64 + r) * 2 + 1];
+        const float M = fmaxf(m_run[t], mo);
+        const float ws = fast_exp2(m_run[t] - M), wo = fast_exp2(mo - M);
+        const float* o_ = ob + ((k - 1) * 64 + r) * OST;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+          acc[t][dt] = acc[t][dt] * ws + *reinterpret_cast<const floatx4*>(o_ + 16 * dt + 4 * g) * wo;
+        n_row[t] = n_row[t] * ws + no * wo;
+        m_run[t] = M;
+      }
     }
   }
-  if (qi < n_q) {
-    const float inv = 1.f / n_row;
-    _Float16* out = P.o + (static_cast<size_t>(qi) * H + h) * D;
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
-      half4 r4;
+  for (int t = 0; t < QT; ++t) {
+    if (qi[t] < n_q) {
+      const float inv = 1.f / n_row[t];
+      _Float16* out = P.o + (static_cast<size_t>(qi[t]) * H + h) * D;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) r4[i] = static_cast<_Float16>(acc[dt][i] * inv);
-      *reinterpret_cast<half4*>(out + 16 * dt + 4 * g) = r4;
+      for (int dt = 0; dt < DT; ++dt) {
+        half4 r4;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) r4[i] = static_cast<_Float16>(acc[t][dt][i] * inv);
+        *reinterpret_cast<half4*>(out + 16 * dt + 4 * g) = r4;
+      }
     }
   }
 }
@@ -1572,12 +1641,16 @@ hipError_t launch_prefill(const PrefillArgs& a, hipStream_t stream) {
   KpfParams P{static_cast<const _Float16*>(a.q), static_cast<_Float16*>(a.o),
               static_cast<const _Float16*>(a.kpool), static_cast<const _Float16*>(a.vpool), a.ss,
               a.hs, a.n_chunks, a.n_q, a.H, a.C, a.qscale};
-  constexpr int kGroups = 2;
-  const dim3 grid((a.n_q + 63) / 64, a.H);
+  // two groups of four wavefronts (16 queries each), two LDS tiles per group
+  constexpr int kGroups = 2, kWaves = 4;
+  const int tiles = ((a.n_q + 63) / 64) * a.H;
+  const dim3 grid(8 * ((tiles + 7) / 8));  // a multiple of the XCD count
   if (a.D == 128)
-    kpf_kernel<128, kGroups><<<grid, 256 * kGroups, 0, stream>>>(P, a.chunk_slot, a.chunk_start);
+    kpf_kernel<128, kGroups, kWaves><<<grid, 64 * kWaves * kGroups, 0, stream>>>(P, a.chunk_slot,
+                                                                                   a.chunk_start);
   else if (a.D == 64)
-    kpf_kernel<64, kGroups><<<grid, 256 * kGroups, 0, stream>>>(P, a.chunk_slot, a.chunk_start);
+    kpf_kernel<64, kGroups, kWaves><<<grid, 64 * kWaves * kGroups, 0, stream>>>(P, a.chunk_slot,
+                                                                                 a.chunk_start);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }
