@@ -147,7 +147,8 @@ struct ca_cache {
   size_t d_cnt_cap = 0;
   PinnedStaging work_stage;     // kernel context uploads
   PinnedStaging prefill_stage;  // prefill paths
-  char* d_path = nullptr;       // prefill path on the device
+  char* d_path = nullptr;       // prefill path on the device (long paths)
+  std::vector<int32_t> prefill_host_path;  // short paths, passed in the kernel arguments
   size_t d_path_cap = 0;
   ca::DevWork dw;
   bool dw_valid = false;
@@ -561,16 +562,26 @@ ca_status ca_prefill_attention(ca_cache* cache, int64_t seq_id, const void* q, v
   if (L > INT32_MAX / 2) return fail(CA_ERR_INVALID, "ca_prefill_attention: sequence too long");
   hipStream_t s = static_cast<hipStream_t>(stream);
 
-  // root -> leaf path: slots and start positions (a chunk may be shorter than c)
+  // root -> leaf path: slots and start positions (a chunk may be shorter
+  // than c). A short path goes to the kernel inside its arguments; a longer
+  // one is uploaded through the pinned staging ring.
   std::vector<int32_t> path;
   for (int32_t id = it->second.term; id != ca::ChunkTree::kRoot; id = cache->tree.node(id).parent)
     path.push_back(id);
   const int32_t nc = static_cast<int32_t>(path.size());
+  const bool inline_path = nc <= ca::kPrefillInlineChunks;
   const size_t bytes = (2 * static_cast<size_t>(nc) + 1) * sizeof(int32_t);
+  std::vector<int32_t>& hp = cache->prefill_host_path;
+  int32_t* slot = nullptr;
   char* h = nullptr;
-  ca_status st = cache->prefill_stage.acquire(bytes, &h);
-  if (st != CA_OK) return st;
-  int32_t* slot = reinterpret_cast<int32_t*>(h);
+  ca_status st = CA_OK;
+  if (inline_path) {
+    hp.resize(2 * static_cast<size_t>(nc) + 1);
+    slot = hp.data();
+  } else {
+    if ((st = cache->prefill_stage.acquire(bytes, &h)) != CA_OK) return st;
+    slot = reinterpret_cast<int32_t*>(h);
+  }
   int32_t* start = slot + nc;
   int32_t pos = 0;
   for (int32_t k = 0; k < nc; ++k) {
@@ -581,9 +592,11 @@ ca_status ca_prefill_attention(ca_cache* cache, int64_t seq_id, const void* q, v
   }
   start[nc] = pos;
   if (pos != L) return fail(CA_ERR_INVALID, "ca_prefill_attention: inconsistent path");
-  if ((st = ensure_device(&cache->d_path, &cache->d_path_cap, bytes, s, "prefill path")) != CA_OK)
-    return st;
-  if ((st = cache->prefill_stage.copy(cache->d_path, bytes, s)) != CA_OK) return st;
+  if (!inline_path) {
+    if ((st = ensure_device(&cache->d_path, &cache->d_path_cap, bytes, s, "prefill path")) != CA_OK)
+      return st;
+    if ((st = cache->prefill_stage.copy(cache->d_path, bytes, s)) != CA_OK) return st;
+  }
 
   ca::PrefillArgs a{};
   a.H = cache->cfg.num_heads;
@@ -595,8 +608,12 @@ ca_status ca_prefill_attention(ca_cache* cache, int64_t seq_id, const void* q, v
   a.vpool = cache->cfg.v_pool;
   a.ss = cache->cfg.slot_stride;
   a.hs = cache->cfg.head_stride;
-  a.chunk_slot = reinterpret_cast<const int32_t*>(cache->d_path);
-  a.chunk_start = a.chunk_slot + nc;
+  if (inline_path) {
+    a.host_path = slot;
+  } else {
+    a.chunk_slot = reinterpret_cast<const int32_t*>(cache->d_path);
+    a.chunk_start = a.chunk_slot + nc;
+  }
   a.n_chunks = nc;
   a.n_q = static_cast<int>(n_q);
   const float sc = scale == 0.f ? 1.f / std::sqrt(static_cast<float>(a.D)) : scale;

@@ -1144,10 +1144,21 @@ __device__ __forceinline__ void kpf_load_chunk(const _Float16* kbase, const _Flo
 template <int D>
 constexpr int kpf_tile_bytes() { return 2 * 64 * kpf_k_stride<D>() * 2; }
 
-template <int D, int NGRP, int WPG>
+// A short path travels inside the kernel arguments (no upload before the
+// launch); NI is its capacity.
+template <int NI>
+struct KpfPath {
+  int32_t slot[NI];
+  int32_t start[NI + 1];
+};
+
+// NI > 0: the path comes in `path` (at most NI chunks); NI == 0: in the
+// device arrays cslot / cstart.
+template <int D, int NGRP, int WPG, int NI>
 __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
-                                                              const int32_t* __restrict__ chunk_slot,
-                                                              const int32_t* __restrict__ chunk_start) {
+                                                              const int32_t* __restrict__ cslot,
+                                                              const int32_t* __restrict__ cstart,
+                                                              const KpfPath<(NI > 0 ? NI : 1)> path) {
   constexpr int QT = 4 / WPG;       // 16-query tiles per wavefront
   constexpr int GT = 64 * WPG;      // threads per group
   constexpr int KS = D / 32;        // 16x16x32 steps over d
@@ -1161,6 +1172,14 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
   static_assert(2 * TB * NGRP <= 160 * 1024, "two LDS tiles per group");
   static_assert(NGRP == 1 || 2 * TB * NGRP >= (NGRP - 1) * 64 * (OST + 2) * 4, "merge buffer");
   __shared__ __attribute__((aligned(16))) char lds[2 * TB * NGRP];
+  auto chunk_slot = [&](int j) -> int {
+    if constexpr (NI > 0) return path.slot[j];
+    else return cslot[j];
+  };
+  auto chunk_start = [&](int j) -> int {
+    if constexpr (NI > 0) return path.start[j];
+    else return cstart[j];
+  };
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int grp = __builtin_amdgcn_readfirstlane((tid >> 6) / WPG);  // uniform: chunk indices stay scalar
@@ -1179,7 +1198,7 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
   const int v = static_cast<int>(blockIdx.x % 8) * per_xcd + static_cast<int>(blockIdx.x / 8);
   if (v >= n_qt * H) return;
   const int h = v / n_qt;
-  const int L = chunk_start[P.n_chunks];
+  const int L = chunk_start(P.n_chunks);
   const int q0 = (v % n_qt) * 64;                              // first query of the tile
   const int pos_last = L - n_q + min(q0 + 63, n_q - 1);        // last position of the tile
   const int pos_first = L - n_q + q0;                          // first position of the tile
@@ -1221,7 +1240,7 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
   const int nc = P.n_chunks;
   int n_ch = 0;
   for (int b = 0; b < nc; b += 64) {
-    const int st = b + lane < nc ? chunk_start[b + lane] : 0x7fffffff;
+    const int st = b + lane < nc ? chunk_start(b + lane) : 0x7fffffff;
     const unsigned long long m = __ballot(st <= pos_last);
     n_ch += __popcll(m);
     if (m != ~0ull) break;
@@ -1234,8 +1253,8 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
   u32x4 kr[GPT], vr[GPT];
   auto issue = [&](int j) {
     j = min(j, n_ch - 1);
-    const int st = chunk_start[j];
-    kpf_load_chunk<D, GT>(kbase, vbase, slot_stride, chunk_slot[j], chunk_start[j + 1] - st, gtid,
+    const int st = chunk_start(j);
+    kpf_load_chunk<D, GT>(kbase, vbase, slot_stride, chunk_slot(j), chunk_start(j + 1) - st, gtid,
                           kr, vr);
   };
   auto stage = [&](int b) {
@@ -1251,8 +1270,8 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
   auto compute = [&](int j, int b) {
     const _Float16* k_lds = tile_k(b);
     const _Float16* v_lds = k_lds + 64 * KST;
-    const int c0 = chunk_start[j];
-    const int len = chunk_start[j + 1] - c0;
+    const int c0 = chunk_start(j);
+    const int len = chunk_start(j + 1) - c0;
 
     // S^T for the chunk's 64 token slots: tile jt holds tokens 16jt..16jt+15;
     // each K read feeds the wavefront's QT query tiles
@@ -1645,12 +1664,24 @@ hipError_t launch_prefill(const PrefillArgs& a, hipStream_t stream) {
   constexpr int kGroups = 2, kWaves = 4;
   const int tiles = ((a.n_q + 63) / 64) * a.H;
   const dim3 grid(8 * ((tiles + 7) / 8));  // a multiple of the XCD count
+  const dim3 block(64 * kWaves * kGroups);
+  if (a.host_path && a.n_chunks <= kPrefillInlineChunks) {
+    KpfPath<kPrefillInlineChunks> path;
+    for (int j = 0; j < a.n_chunks; ++j) path.slot[j] = a.host_path[j];
+    for (int j = 0; j <= a.n_chunks; ++j) path.start[j] = a.host_path[a.n_chunks + j];
+    if (a.D == 128)
+      kpf_kernel<128, kGroups, kWaves, kPrefillInlineChunks><<<grid, block, 0, stream>>>(P, nullptr, nullptr, path);
+    else if (a.D == 64)
+      kpf_kernel<64, kGroups, kWaves, kPrefillInlineChunks><<<grid, block, 0, stream>>>(P, nullptr, nullptr, path);
+    else return hipErrorInvalidValue;
+    return hipGetLastError();
+  }
+  if (!a.chunk_slot) return hipErrorInvalidValue;
+  const KpfPath<1> none{};
   if (a.D == 128)
-    kpf_kernel<128, kGroups, kWaves><<<grid, 64 * kWaves * kGroups, 0, stream>>>(P, a.chunk_slot,
-                                                                                   a.chunk_start);
+    kpf_kernel<128, kGroups, kWaves, 0><<<grid, block, 0, stream>>>(P, a.chunk_slot, a.chunk_start, none);
   else if (a.D == 64)
-    kpf_kernel<64, kGroups, kWaves><<<grid, 64 * kWaves * kGroups, 0, stream>>>(P, a.chunk_slot,
-                                                                                 a.chunk_start);
+    kpf_kernel<64, kGroups, kWaves, 0><<<grid, block, 0, stream>>>(P, a.chunk_slot, a.chunk_start, none);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }

@@ -61,7 +61,10 @@ hipError_t launch_attention(const AttnArgs& a, const DevWork& w, hipStream_t str
                             int phase_mask, const SideStream& side);
 
 // Causal prefill attention of a sequence's last n_q tokens over its path
-// (fp16 only). chunk_slot/chunk_start are device arrays of the path.
+// (fp16 only). A path of at most kPrefillInlineChunks chunks is passed from
+// host_path (slots, then starts) inside the kernel arguments; a longer one
+// through the device arrays chunk_slot/chunk_start.
+constexpr int kPrefillInlineChunks = 255;
 struct PrefillArgs {
   int H, D, C;
   const void* q;
@@ -69,8 +72,9 @@ struct PrefillArgs {
   const void* kpool;
   const void* vpool;
   int64_t ss, hs;              // pool strides of a slot and of a head (elements)
-  const int32_t* chunk_slot;   // [n_chunks]
-  const int32_t* chunk_start;  // [n_chunks + 1]
+  const int32_t* host_path;    // host [n_chunks] slots then [n_chunks + 1] starts, or null
+  const int32_t* chunk_slot;   // device [n_chunks] (paths longer than the inline limit)
+  const int32_t* chunk_start;  // device [n_chunks + 1]
   int n_chunks;
   int n_q;
   float qscale;  // softmax scale * log2(e)

@@ -91,3 +91,23 @@ def test_prefill_errors_and_noop():
     p32.insert(0, toks, k32, v32)
     with pytest.raises(ChunkAttnError):
         p32.cache.prefill(0, to_dev(np.zeros((3, 2, 64), np.float32)))
+
+
+@pytest.mark.parametrize("c,L", [(1, 255), (1, 256), (2, 700)])
+def test_prefill_long_paths(c, L):
+    """Paths of up to 255 chunks travel in the kernel arguments, longer ones
+    through a device upload: both sides of that limit, and a long path of
+    short chunks."""
+    print(f"[case] prefill path of {-(-L // c)} chunks (c={c}, L={L})", flush=True)
+    H, d = 2, 64
+    rng = np.random.default_rng(900 + L)
+    p = Pair(c, H, d, np.float16, 2048)
+    toks = rng.integers(0, 50, L).astype(np.int32)
+    k, v = prefix_keyed_kv(7, toks, 0, H, d, np.float16)
+    p.insert(0, toks, k, v)
+    for n_q in (1, 70, L):
+        q = rng.standard_normal((n_q, H, d)).astype(np.float16)
+        o = p.cache.prefill(0, to_dev(q))
+        torch.cuda.synchronize()
+        ref = prefill_attention(p.tree, 0, q, 1.0 / np.sqrt(d))
+        assert_close(o.cpu().numpy(), ref, np.float16, f"prefill c={c} L={L} n_q={n_q}")
