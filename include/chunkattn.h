@@ -207,7 +207,8 @@ ca_status ca_attention(ca_cache* cache, const void* q, void* o, float scale, voi
  *   scale  softmax scale applied to q.k; 0 means 1/sqrt(d)
  * fp16 caches only. Enqueue on the stream of the insert/extend that wrote
  * the K/V rows. The path (chunk slots and start positions, 8 bytes per
- * chunk) is copied to the device through library-owned pinned staging.
+ * chunk) travels inside the kernel arguments for up to 255 chunks; a longer
+ * one is copied to the device through library-owned pinned staging.
  * Errors: INVALID (table-only or fp32 cache, null or misaligned q/o,
  * n_q > L), NOT_FOUND, DEVICE. */
 ca_status ca_prefill_attention(ca_cache* cache, int64_t seq_id, const void* q, void* o,
