@@ -1122,27 +1122,29 @@ struct KpfParams {
 template <int D>
 constexpr int kpf_k_stride() { return D + 8; }   // halves per K (and V) row in LDS
 
-// One chunk's K and V rows for a group of GT threads: granule e = tid + GT*u
-// is token e / (D/8), 16-byte column e % (D/8) (coalesced rows). Rows past
-// the chunk's length re-read its last row (their scores are masked).
-template <int D, int GT>
-__device__ __forceinline__ void kpf_load_chunk(const _Float16* kbase, const _Float16* vbase,
-                                               size_t slot_stride, int slot, int len, int tid,
-                                               u32x4 (&kr)[D * 8 / GT], u32x4 (&vr)[D * 8 / GT]) {
+// TOK rows of a chunk's K and V (rows r0 .. r0 + TOK - 1) for a group of GT
+// threads: granule e = tid + GT*u is row r0 + e / (D/8), 16-byte column
+// e % (D/8) (coalesced rows). Rows past the chunk's length re-read its last
+// row (their scores are masked).
+template <int D, int GT, int TOK>
+__device__ __forceinline__ void kpf_load_rows(const _Float16* kbase, const _Float16* vbase,
+                                              size_t slot_stride, int slot, int r0, int len, int tid,
+                                              u32x4 (&kr)[TOK * D / 8 / GT],
+                                              u32x4 (&vr)[TOK * D / 8 / GT]) {
   constexpr int NG = D / 8;
   const _Float16* kb = kbase + slot * slot_stride;
   const _Float16* vb = vbase + slot * slot_stride;
 #pragma unroll
-  for (int u = 0; u < D * 8 / GT; ++u) {
+  for (int u = 0; u < TOK * NG / GT; ++u) {
     const int e = tid + GT * u;
-    const size_t off = static_cast<size_t>(min(e / NG, len - 1)) * D + (e % NG) * 8;
+    const size_t off = static_cast<size_t>(min(r0 + e / NG, len - 1)) * D + (e % NG) * 8;
     kr[u] = *reinterpret_cast<const u32x4*>(kb + off);
     vr[u] = *reinterpret_cast<const u32x4*>(vb + off);
   }
 }
 
-template <int D>
-constexpr int kpf_tile_bytes() { return 2 * 64 * kpf_k_stride<D>() * 2; }
+template <int D, int TOK>
+constexpr int kpf_tile_bytes() { return 2 * TOK * kpf_k_stride<D>() * 2; }
 
 // A short path travels inside the kernel arguments (no upload before the
 // launch); NI is its capacity.
@@ -1152,9 +1154,10 @@ struct KpfPath {
   int32_t start[NI + 1];
 };
 
-// NI > 0: the path comes in `path` (at most NI chunks); NI == 0: in the
-// device arrays cslot / cstart.
-template <int D, int NGRP, int WPG, int NI>
+// Work unit: TOK consecutive rows of one chunk (a chunk of up to c tokens
+// has ceil(c / TOK) units). NI > 0: the path comes in `path` (at most NI
+// chunks); NI == 0: in the device arrays cslot / cstart.
+template <int D, int NGRP, int WPG, int TOK, int NI>
 __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
                                                               const int32_t* __restrict__ cslot,
                                                               const int32_t* __restrict__ cstart,
@@ -1164,11 +1167,14 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
   constexpr int KS = D / 32;        // 16x16x32 steps over d
   constexpr int DT = D / 16;        // 16-wide d tiles of O^T
   constexpr int NG = D / 8;         // 16-byte granules per token row
-  constexpr int GPT = 64 * NG / GT; // granules of K (and of V) per thread per chunk
+  constexpr int GPT = TOK * NG / GT;// granules of K (and of V) per thread per unit
+  constexpr int JT = TOK / 16;      // 16-token tiles of S^T per unit
+  constexpr int PV = TOK / 32;      // 32-token steps of O^T per unit
   constexpr int KST = kpf_k_stride<D>();
-  constexpr int TB = kpf_tile_bytes<D>();
+  constexpr int TB = kpf_tile_bytes<D, TOK>();
   constexpr int OST = D + 4;         // merge buffer row stride (floats): rows start 4 banks apart
   static_assert(WPG * QT == 4, "64 queries per block");
+  static_assert(TOK % 32 == 0 && TOK <= 64 && GPT * GT == TOK * NG, "unit shape");
   static_assert(2 * TB * NGRP <= 160 * 1024, "two LDS tiles per group");
   static_assert(NGRP == 1 || 2 * TB * NGRP >= (NGRP - 1) * 64 * (OST + 2) * 4, "merge buffer");
   __shared__ __attribute__((aligned(16))) char lds[2 * TB * NGRP];
@@ -1182,7 +1188,7 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
   };
 
   const int tid = threadIdx.x, lane = tid & 63;
-  const int grp = __builtin_amdgcn_readfirstlane((tid >> 6) / WPG);  // uniform: chunk indices stay scalar
+  const int grp = __builtin_amdgcn_readfirstlane((tid >> 6) / WPG);  // uniform: unit indices stay scalar
   const int w = (tid >> 6) % WPG;   // wavefront inside the group
   const int gtid = tid % GT;        // thread index inside the group
   const int l16 = lane & 15, g = lane >> 4;
@@ -1205,6 +1211,7 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
   const size_t slot_stride = static_cast<size_t>(P.ss);
   const _Float16* kbase = P.kpool + h * P.hs;
   const _Float16* vbase = P.vpool + h * P.hs;
+  const int upc = (P.C + TOK - 1) / TOK;                       // units per chunk
 
   // this lane's query row of tile t, and its position
   int qi[QT], pos[QT];
@@ -1223,7 +1230,7 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
     }
   }
   // q has arrived before any chunk load is issued, so the MFMAs inside the
-  // loop never wait on vector memory (the next chunk's loads stay in flight)
+  // loop never wait on vector memory (the next unit's loads stay in flight)
   wait_stores();
   float m_run[QT], n_part[QT];
   floatx4 acc[QT][DT];
@@ -1245,21 +1252,23 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
     n_ch += __popcll(m);
     if (m != ~0ull) break;
   }
+  const int n_units = n_ch * upc;
   // Per-chunk metadata comes through the scalar cache (uniform index,
-  // read-only arguments), so no metadata load ever waits behind the chunk
-  // rows in flight. Past the end the registers reload the group's last
-  // chunk: every step issues the same loads, so the wait before each LDS
-  // write covers exactly the registers it needs on every path.
+  // read-only arguments), so no metadata load ever waits behind the rows in
+  // flight. Past the end the registers reload the last unit: every step
+  // issues the same loads, so the wait before each LDS write covers exactly
+  // the registers it needs on every path.
   u32x4 kr[GPT], vr[GPT];
-  auto issue = [&](int j) {
-    j = min(j, n_ch - 1);
+  auto issue = [&](int u) {
+    u = min(u, n_units - 1);
+    const int j = u / upc;
     const int st = chunk_start(j);
-    kpf_load_chunk<D, GT>(kbase, vbase, slot_stride, chunk_slot(j), chunk_start(j + 1) - st, gtid,
-                          kr, vr);
+    kpf_load_rows<D, GT, TOK>(kbase, vbase, slot_stride, chunk_slot(j), TOK * (u % upc),
+                              chunk_start(j + 1) - st, gtid, kr, vr);
   };
   auto stage = [&](int b) {
     _Float16* k_lds = tile_k(b);
-    _Float16* v_lds = k_lds + 64 * KST;
+    _Float16* v_lds = k_lds + TOK * KST;
 #pragma unroll
     for (int u = 0; u < GPT; ++u) {
       const int e = gtid + GT * u;
@@ -1267,17 +1276,20 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
       *reinterpret_cast<u32x4*>(v_lds + (e / NG) * KST + (e % NG) * 8) = vr[u];
     }
   };
-  auto compute = [&](int j, int b) {
+  auto compute = [&](int u, int b) {
     const _Float16* k_lds = tile_k(b);
-    const _Float16* v_lds = k_lds + 64 * KST;
-    const int c0 = chunk_start(j);
-    const int len = chunk_start(j + 1) - c0;
+    const _Float16* v_lds = k_lds + TOK * KST;
+    const int j = u / upc;
+    const int r0 = TOK * (u % upc);
+    const int c0 = chunk_start(j) + r0;                     // position of the unit's first row
+    const int len = min(TOK, chunk_start(j + 1) - c0);      // rows of the unit
+    if (len <= 0 || c0 > pos_last) return;                  // nothing the tile can see (uniform)
 
-    // S^T for the chunk's 64 token slots: tile jt holds tokens 16jt..16jt+15;
+    // S^T for the unit's token slots: tile jt holds tokens 16jt..16jt+15;
     // each K read feeds the wavefront's QT query tiles
-    floatx4 sacc[QT][4];
+    floatx4 sacc[QT][JT];
 #pragma unroll
-    for (int jt = 0; jt < 4; ++jt) {
+    for (int jt = 0; jt < JT; ++jt) {
 #pragma unroll
       for (int t = 0; t < QT; ++t) sacc[t][jt] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -1289,27 +1301,27 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
       }
     }
     // lane holds S^T[token 16jt + 4g + i][row l16 of tile t] (unscaled).
-    // Chunks that are whole and end before the tile's first position need
-    // no mask (uniform test).
-    if (len < 64 || c0 + 63 > pos_first) {
+    // Units that are whole and end before the tile's first position need no
+    // mask (uniform test).
+    if (len < TOK || c0 + TOK - 1 > pos_first) {
 #pragma unroll
       for (int t = 0; t < QT; ++t)
 #pragma unroll
-        for (int jt = 0; jt < 4; ++jt)
+        for (int jt = 0; jt < JT; ++jt)
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const int tk = 16 * jt + 4 * g + i;
             if (!(tk < len && c0 + tk <= pos[t])) sacc[t][jt][i] = -INFINITY;
           }
     }
-    half8 pb[QT][2];
+    half8 pb[QT][PV];
     bool moved = false;
     float alpha[QT];
 #pragma unroll
     for (int t = 0; t < QT; ++t) {
       float lmax = -INFINITY;
 #pragma unroll
-      for (int jt = 0; jt < 4; ++jt)
+      for (int jt = 0; jt < JT; ++jt)
 #pragma unroll
         for (int i = 0; i < 4; ++i) lmax = fmaxf(lmax, sacc[t][jt][i]);
       lmax = fmaxf(lmax, __shfl_xor(lmax, 16));
@@ -1319,10 +1331,10 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
       alpha[t] = fast_exp2(m_run[t] - mn);
       moved |= alpha[t] != 1.f;
       m_run[t] = mn;
-      half4 ph[4];
+      half4 ph[JT];
       float ps = 0.f;
 #pragma unroll
-      for (int jt = 0; jt < 4; ++jt) {
+      for (int jt = 0; jt < JT; ++jt) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const float pv = fast_exp2(__builtin_fmaf(sacc[t][jt][i], P.qscale, -mn));
@@ -1337,7 +1349,7 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
       // exactly what the lane holds of P^T; two transposing reads fetch the
       // V^T side.
 #pragma unroll
-      for (int p2 = 0; p2 < 2; ++p2)
+      for (int p2 = 0; p2 < PV; ++p2)
         pb[t][p2] = __builtin_shufflevector(ph[2 * p2], ph[2 * p2 + 1], 0, 1, 2, 3, 4, 5, 6, 7);
     }
     // O is rescaled only when some row's maximum moved (uniform test)
@@ -1350,7 +1362,7 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
 #pragma unroll
-      for (int p2 = 0; p2 < 2; ++p2) {
+      for (int p2 = 0; p2 < PV; ++p2) {
         const _Float16* vp = v_lds + (32 * p2 + 4 * g + (l16 >> 2)) * KST + 16 * dt + 4 * (l16 & 3);
         const half4 v0 = lds_read_tr16(vp);             // tokens 32p + 4g + j
         const half4 v1 = lds_read_tr16(vp + 16 * KST);  // tokens 32p + 16 + 4g + j
@@ -1361,11 +1373,11 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
       }
     }
   };
-  // Two LDS tiles per group: step i computes the group's chunk i from tile
-  // i % 2 while chunk i + 1 is written into the other tile and chunk i + 2
+  // Two LDS tiles per group: step i computes the group's unit i from tile
+  // i % 2 while unit i + 1 is written into the other tile and unit i + 2
   // loads into the registers; one barrier per step (after it, tile i % 2 is
   // complete and nobody still reads the other one).
-  const int steps = (n_ch + NGRP - 1) / NGRP;  // the same in every group
+  const int steps = (n_units + NGRP - 1) / NGRP;  // the same in every group
   if (steps > 0) {
     issue(grp);
     stage(0);
@@ -1377,8 +1389,8 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
       stage((i + 1) & 1);
       issue(grp + (i + 2) * NGRP);
     }
-    const int j = grp + i * NGRP;
-    if (j < n_ch) compute(j, i & 1);
+    const int u = grp + i * NGRP;
+    if (u < n_units) compute(u, i & 1);
   }
   // row sums over the four lane groups
   float n_row[QT];
@@ -1660,8 +1672,9 @@ hipError_t launch_prefill(const PrefillArgs& a, hipStream_t stream) {
   KpfParams P{static_cast<const _Float16*>(a.q), static_cast<_Float16*>(a.o),
               static_cast<const _Float16*>(a.kpool), static_cast<const _Float16*>(a.vpool), a.ss,
               a.hs, a.n_chunks, a.n_q, a.H, a.C, a.qscale};
-  // two groups of four wavefronts (16 queries each), two LDS tiles per group
-  constexpr int kGroups = 2, kWaves = 4;
+  // two groups of four wavefronts (16 queries each), 64-row units, two LDS
+  // tiles per group
+  constexpr int kGroups = 2, kWaves = 4, kTok = 64;
   const int tiles = ((a.n_q + 63) / 64) * a.H;
   const dim3 grid(8 * ((tiles + 7) / 8));  // a multiple of the XCD count
   const dim3 block(64 * kWaves * kGroups);
@@ -1670,18 +1683,22 @@ hipError_t launch_prefill(const PrefillArgs& a, hipStream_t stream) {
     for (int j = 0; j < a.n_chunks; ++j) path.slot[j] = a.host_path[j];
     for (int j = 0; j <= a.n_chunks; ++j) path.start[j] = a.host_path[a.n_chunks + j];
     if (a.D == 128)
-      kpf_kernel<128, kGroups, kWaves, kPrefillInlineChunks><<<grid, block, 0, stream>>>(P, nullptr, nullptr, path);
+      kpf_kernel<128, kGroups, kWaves, kTok, kPrefillInlineChunks><<<grid, block, 0, stream>>>(
+          P, nullptr, nullptr, path);
     else if (a.D == 64)
-      kpf_kernel<64, kGroups, kWaves, kPrefillInlineChunks><<<grid, block, 0, stream>>>(P, nullptr, nullptr, path);
+      kpf_kernel<64, kGroups, kWaves, kTok, kPrefillInlineChunks><<<grid, block, 0, stream>>>(
+          P, nullptr, nullptr, path);
     else return hipErrorInvalidValue;
     return hipGetLastError();
   }
   if (!a.chunk_slot) return hipErrorInvalidValue;
   const KpfPath<1> none{};
   if (a.D == 128)
-    kpf_kernel<128, kGroups, kWaves, 0><<<grid, block, 0, stream>>>(P, a.chunk_slot, a.chunk_start, none);
+    kpf_kernel<128, kGroups, kWaves, kTok, 0><<<grid, block, 0, stream>>>(P, a.chunk_slot,
+                                                                         a.chunk_start, none);
   else if (a.D == 64)
-    kpf_kernel<64, kGroups, kWaves, 0><<<grid, block, 0, stream>>>(P, a.chunk_slot, a.chunk_start, none);
+    kpf_kernel<64, kGroups, kWaves, kTok, 0><<<grid, block, 0, stream>>>(P, a.chunk_slot,
+                                                                        a.chunk_start, none);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }

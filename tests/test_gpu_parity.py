@@ -173,6 +173,48 @@ def test_random_trees(seed):
             assert_close(o, ref, dtype, f"random tree seed={seed} op={i}")
 
 
+@pytest.mark.parametrize("c,dtype", [(128, np.float16), (100, np.float16), (65, np.float32),
+                                     (200, np.float16)])
+def test_random_trees_long_chunks(c, dtype):
+    """Chunks longer than the kernels' 64-token blocks: every chunk spans
+    several blocks, the last one ragged."""
+    seed = 40 + c
+    d, H = 128 if c % 2 == 0 else 64, 2
+    print(f"[case] long chunks c={c} dtype={np.dtype(dtype).name}", flush=True)
+    p = Pair(c, H, d, dtype, 1024)
+    full = {}
+    qrng = np.random.default_rng(2000 + seed)
+    ops = random_op_script(seed, n_ops=30, alphabet=3, max_len=2 * c + 40)
+    for i, op in enumerate(ops):
+        if op[0] == "insert":
+            k, v = prefix_keyed_kv(seed, op[2], 0, H, d, dtype)
+            p.insert(op[1], op[2], k, v)
+            full[op[1]] = np.asarray(op[2], np.int32)
+        elif op[0] == "extend":
+            toks = np.concatenate([full[op[1]], op[2]]).astype(np.int32)
+            k, v = prefix_keyed_kv(seed, toks, len(full[op[1]]), H, d, dtype)
+            p.extend(op[1], op[2], k, v)
+            full[op[1]] = toks
+        elif op[0] == "append":
+            ks, vs = [], []
+            for sid, tok in zip(op[1], op[2]):
+                toks = np.concatenate([full[sid], [tok]]).astype(np.int32)
+                k, v = prefix_keyed_kv(seed, toks, len(full[sid]), H, d, dtype)
+                ks.append(k)
+                vs.append(v)
+                full[sid] = toks
+            p.append(op[1], op[2], np.concatenate(ks), np.concatenate(vs))
+        else:
+            p.remove(op[1])
+            del full[op[1]]
+        if full and (i % 5 == 4 or i == len(ops) - 1):
+            p.check_tables()
+            qmap = {sid: qrng.standard_normal((H, d)).astype(np.float32).astype(dtype) for sid in full}
+            o, q, row_seq = p.attention(qmap)
+            ref = p.reference(row_seq, q, 0.0)
+            assert_close(o, ref, dtype, f"long chunks c={c} op={i}")
+
+
 def _small_pair(c=4, H=2, d=64, dtype=np.float16):
     return Pair(c, H, d, dtype, 256)
 

@@ -43,12 +43,13 @@ def test_join_single_prompt_tree_512_new_tokens():
     assert np.abs(od[r].astype(np.float64) - o[-1].cpu().numpy().astype(np.float64)).max() < 2e-3
 
 
-@pytest.mark.parametrize("case", range(10))
+@pytest.mark.parametrize("case", range(13))
 def test_prefill_random_trees(case):
     """Shared prefixes that split chunks mid-way, short chunks on the path,
-    n_q from 1 to the whole sequence, both head sizes and both pool layouts."""
+    chunks longer than 64 tokens, n_q from 1 to the whole sequence, both head
+    sizes and both pool layouts."""
     rng = np.random.default_rng(500 + case)
-    c = [1, 3, 4, 7, 16, 64, 5, 64, 16, 2][case]
+    c = [1, 3, 4, 7, 16, 64, 5, 64, 16, 2, 128, 100, 65][case]
     d = [64, 128][case % 2]
     H = 1 + case % 3
     layout = "interleaved" if case % 4 == 3 else "split"
