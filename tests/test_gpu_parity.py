@@ -177,11 +177,14 @@ def test_random_trees(seed):
                                      (200, np.float16)])
 def test_random_trees_long_chunks(c, dtype):
     """Chunks longer than the kernels' 64-token blocks: every chunk spans
-    several blocks, the last one ragged."""
+    several blocks, the last one ragged (c=100 under the partial-free
+    schedule)."""
     seed = 40 + c
     d, H = 128 if c % 2 == 0 else 64, 2
     print(f"[case] long chunks c={c} dtype={np.dtype(dtype).name}", flush=True)
     p = Pair(c, H, d, dtype, 1024)
+    if c == 100:  # the partial-free schedule, one segment per chunk
+        p.cache.set_tuning(seg_chunks=1, schedule=4)
     full = {}
     qrng = np.random.default_rng(2000 + seed)
     ops = random_op_script(seed, n_ops=30, alphabet=3, max_len=2 * c + 40)
