@@ -233,8 +233,10 @@ ca_status ca_stats(const ca_cache* cache, int64_t* uploads, int64_t* slots_used,
 /* Tuning and per-phase measurement (schedules change speed, not results).
  *   seg_chunks   shared chunks per chunk-first work item (1..64; 0 keeps the
  *                current value; -1, the default, sizes segments for about
- *                one chunk-first block per compute unit, at most 16 chunks).
- *                More chunks per item mean fewer partials.
+ *                one chunk-first block per compute unit, at most 16 chunks
+ *                unless the private K/V stream is long enough to hide longer
+ *                chains, then up to 64). More chunks per item mean fewer
+ *                partials.
  *   schedule     0: chunk-first launch, then a sequence-first launch whose
  *                items fold the chunk-first partials; 1: both phases in one
  *                launch (chunk-first items first), every item writes a

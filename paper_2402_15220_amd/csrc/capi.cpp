@@ -169,6 +169,7 @@ struct ca_cache {
   }
 
   size_t esize() const { return cfg.dtype == CA_FP16 ? 2 : 4; }
+  int32_t token_head_bytes() const { return static_cast<int32_t>(2 * cfg.head_dim * esize()); }
 
   // Work lists for the current tree. Decode growth (new private chunks at
   // the end of paths) patches them in place (Section 3.3's context stays
@@ -185,15 +186,16 @@ struct ca_cache {
         ca::Tables t;
         ca::WorkLists full;
         ca::build_tables(tree, &t);
-        ca::build_work(tree, t, seg_chunks, split_chunks, schedule != 0, cfg.num_heads, num_cus,
-                       &full, schedule == 4);
+        // patched lists keep the segment size of their last rebuild
+        ca::build_work(tree, t, work.seg_chunks, split_chunks, schedule != 0, cfg.num_heads,
+                       num_cus, &full, schedule == 4, token_head_bytes());
         const char* d = ca::same_work(work, full);
         if (*d) patch_error = std::string("work-list patch differs from a rebuild: ") + d;
       }
     } else {
       ca::build_tables(tree, &tables);
       ca::build_work(tree, tables, seg_chunks, split_chunks, schedule != 0, cfg.num_heads, num_cus,
-                     &work, schedule == 4);
+                     &work, schedule == 4, token_head_bytes());
     }
     work_valid = true;
     dw_valid = false;

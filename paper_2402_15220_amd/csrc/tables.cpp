@@ -106,7 +106,7 @@ void build_tables(const ChunkTree& tree, Tables* out) {
 
 void build_work(const ChunkTree& tree, const Tables& T, int32_t seg_chunks, int32_t split_chunks,
                 bool partial_items, int32_t num_heads, int32_t num_cus, WorkLists* out,
-                bool serial_reduce) {
+                bool serial_reduce, int32_t token_head_bytes) {
   WorkLists& W = *out;
   if (serial_reduce) {
     // every segment is one more launch: by default a run is one segment
@@ -136,15 +136,23 @@ void build_work(const ChunkTree& tree, const Tables& T, int32_t seg_chunks, int3
 
   // Automatic segment size: about one chunk-first block per compute unit,
   // counting a run of L chunks over r rows as L * ceil(r/16) * H chunk-blocks
-  // (16 rows per block in the fused launch); at most 16 chunks per segment.
+  // (16 rows per block in the fused launch). A segment is a chain of
+  // dependent chunk steps, so segments stay at 16 chunks or fewer unless the
+  // sequence-first stream (the private K/V at ~6 TB/s) is long enough to hide
+  // a longer chain at ~3 us per chunk under load; longer segments mean fewer
+  // partials per row.
   if (seg_chunks <= 0) {
     int64_t work = 0;
     for (const auto& chain : runs) {
       const int64_t r = T.node_row_end[chain[0]] - T.node_row_begin[chain[0]];
       work += static_cast<int64_t>(chain.size()) * ((r + 15) / 16) * num_heads;
     }
+    int64_t priv_tokens = 0;
+    for (int32_t k : T.priv_node) priv_tokens += T.node_len[k];
+    const double ksf_us = static_cast<double>(priv_tokens) * num_heads * token_head_bytes / 6.0e6;
+    const int64_t cap = std::min<int64_t>(64, std::max<int64_t>(16, static_cast<int64_t>(ksf_us / 3.0)));
     const int64_t cus = num_cus > 0 ? num_cus : 256;
-    seg_chunks = static_cast<int32_t>(std::min<int64_t>(16, std::max<int64_t>(1, (work + cus - 1) / cus)));
+    seg_chunks = static_cast<int32_t>(std::min<int64_t>(cap, std::max<int64_t>(1, (work + cus - 1) / cus)));
   }
   if (seg_chunks > 64) seg_chunks = 64;  // the chunk-first kernel keeps a segment's slots in lanes
   W.seg_chunks = seg_chunks;

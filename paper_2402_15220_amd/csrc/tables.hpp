@@ -71,9 +71,11 @@ struct WorkLists {
 // that order (seg_group_ptr), so no row has two writers at once; segments
 // take up to 64 chunks (seg_chunks <= 0) and pad0 = 1 marks the ones that
 // fold (not the first on their rows' paths).
+// token_head_bytes: K+V bytes of one token of one head (2·d·element size),
+// used by the automatic segment size to estimate the sequence-first stream.
 void build_work(const ChunkTree& tree, const Tables& t, int32_t seg_chunks, int32_t split_chunks,
                 bool partial_items, int32_t num_heads, int32_t num_cus, WorkLists* out,
-                bool serial_reduce = false);
+                bool serial_reduce = false, int32_t token_head_bytes = 512);
 
 // Bring work lists built for an earlier tree up to date when the only
 // structural changes since were new private chunks at the end of sequences'
