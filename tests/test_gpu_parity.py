@@ -218,6 +218,31 @@ def test_random_trees_long_chunks(c, dtype):
             assert_close(o, ref, dtype, f"long chunks c={c} op={i}")
 
 
+@pytest.mark.parametrize("sched", [0, 1, 2, 4])
+def test_deep_tree_many_partials(sched):
+    """A comb of 80 sequences, sequence k sharing its first k two-token chunks
+    with every longer one: each chunk covers a different row range, so with
+    one chunk per segment the longest rows fold 79 partials (more than one
+    64-wide batch of the merge)."""
+    print(f"[case] deep tree schedule={sched}", flush=True)
+    c, H, d = 2, 2, 64
+    rng = np.random.default_rng(77)
+    base = rng.integers(0, 30, 2 * 80).astype(np.int32)
+    p = Pair(c, H, d, np.float16, 4096)
+    for k in range(1, 81):
+        toks = np.concatenate([base[:2 * k], [1000 + k]]).astype(np.int32)
+        kk, vv = prefix_keyed_kv(77, toks, 0, H, d, np.float16)
+        p.insert(k, toks, kk, vv)
+    p.cache.set_tuning(seg_chunks=1, split_chunks=0, schedule=sched)
+    p.check_tables()
+    qrng = np.random.default_rng(78)
+    qmap = {k: qrng.standard_normal((H, d)).astype(np.float16) for k in range(1, 81)}
+    for rep in range(2):
+        o, q, row_seq = p.attention(qmap)
+        ref = p.reference(row_seq, q, 0.0) if rep == 0 else ref
+        assert_close(o, ref, np.float16, f"deep tree schedule={sched} rep={rep}")
+
+
 def _small_pair(c=4, H=2, d=64, dtype=np.float16):
     return Pair(c, H, d, dtype, 256)
 
