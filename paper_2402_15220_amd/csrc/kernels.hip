@@ -1293,20 +1293,27 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
     if (len <= 0 || c0 > pos_last) return;                  // nothing the tile can see (uniform)
 
     // S^T for the unit's token slots: tile jt holds tokens 16jt..16jt+15;
-    // each K read feeds the wavefront's QT query tiles
+    // each K read feeds the wavefront's QT query tiles. All of the unit's K
+    // fragments are read first (one wait), then the JT independent
+    // accumulation chains are interleaved on the matrix cores.
     floatx4 sacc[QT][JT];
+    half8 ka[JT][KS];
 #pragma unroll
-    for (int jt = 0; jt < JT; ++jt) {
+    for (int jt = 0; jt < JT; ++jt)
+#pragma unroll
+      for (int s = 0; s < KS; ++s)
+        ka[jt][s] = *reinterpret_cast<const half8*>(k_lds + (16 * jt + l16) * KST + 32 * s + 8 * g);
+#pragma unroll
+    for (int jt = 0; jt < JT; ++jt)
 #pragma unroll
       for (int t = 0; t < QT; ++t) sacc[t][jt] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        const half8 ka = *reinterpret_cast<const half8*>(k_lds + (16 * jt + l16) * KST + 32 * s + 8 * g);
+    for (int s = 0; s < KS; ++s)
+#pragma unroll
+      for (int jt = 0; jt < JT; ++jt)
 #pragma unroll
         for (int t = 0; t < QT; ++t)
-          sacc[t][jt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ka, qf[t][s], sacc[t][jt], 0, 0, 0);
-      }
-    }
+          sacc[t][jt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ka[jt][s], qf[t][s], sacc[t][jt], 0, 0, 0);
     // lane holds S^T[token 16jt + 4g + i][row l16 of tile t] (unscaled).
     // Units that are whole and end before the tile's first position need no
     // mask (uniform test).
