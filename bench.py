@@ -43,7 +43,10 @@ def _parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--config", type=int, default=2, help="workload 2, 3 or 4 (default 2)")
+    ap.add_argument("--config", type=int, default=2,
+                    help="static workload: 2 = one 1024-token prompt shared by 32 rows with 512 "
+                         "unique tokens each (default), 3 = the same with a 4096-token prompt, "
+                         "4 = two-level tree of 64 rows")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle sample time")
     ap.add_argument("--no-cold", action="store_true", help="skip the cache-evicted timing")

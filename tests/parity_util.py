@@ -9,7 +9,7 @@ import torch
 from oracle import OracleTree, dense_attention_rows, tables
 from paper_2402_15220_amd.cache import Cache
 
-# the benchmark spec bar for fp16 inputs with fp32 accumulation
+# parity bar for fp16 inputs with fp32 accumulation (max-abs and relative L2)
 FP16_MAX_ABS = 2e-3
 FP16_REL_L2 = 1e-3
 # fp32 inputs: fp32 products and sums over at most a few thousand terms

@@ -39,14 +39,14 @@ def _static_pair(wl, slack=16, layout="split"):
                                         (1, "interleaved"), (2, "interleaved")])
 def test_static_config(cfg, layout):
     """Full-size static trees; K/V pools split (default) and interleaved."""
-    print(f"[case] static config {cfg} layout={layout}", flush=True)
     wl = make_static(cfg)
+    print(f"[case] {wl.name} layout={layout}", flush=True)
     p = _static_pair(wl, layout=layout)
     tb = p.check_tables()
     p.check_pool(max_nodes=48)
     o, q, row_seq = p.attention({s.seq_id: wl.q[s.seq_id] for s in wl.seqs})
     ref = p.reference(row_seq, q, 0.0)
-    assert_close(o, ref, wl.dtype, f"config {cfg} (B={tb['row_seq'].shape[0]})")
+    assert_close(o, ref, wl.dtype, f"{wl.name} (B={tb['row_seq'].shape[0]})")
 
 
 @pytest.mark.parametrize("seg,split,sched", [(1, 0, 0), (16, 0, 0), (4, 3, 0), (2, 1, 0), (64, 5, 0),
@@ -56,14 +56,14 @@ def test_static_config(cfg, layout):
 def test_config2_work_partitions(seg, split, sched):
     """Every schedule, segment size and split gives the same result, and
     repeated calls (counters reset by the kernels) stay correct."""
-    print(f"[case] config 2 seg={seg} split={split} schedule={sched}", flush=True)
+    print(f"[case] single-prompt tree seg={seg} split={split} schedule={sched}", flush=True)
     wl = make_static(2)
     p = _static_pair(wl)
     p.cache.set_tuning(seg_chunks=seg, split_chunks=split, schedule=sched)
     for rep in range(3):
         o, q, row_seq = p.attention({s.seq_id: wl.q[s.seq_id] for s in wl.seqs})
         ref = p.reference(row_seq, q, 0.0) if rep == 0 else ref
-        assert_close(o, ref, wl.dtype, f"config 2 seg={seg} split={split} schedule={sched} rep={rep}")
+        assert_close(o, ref, wl.dtype, f"single-prompt tree seg={seg} split={split} schedule={sched} rep={rep}")
 
 
 @pytest.mark.parametrize("cfg,seg", [(3, -1), (4, -1), (4, 1)])
@@ -71,20 +71,20 @@ def test_partial_free_multi_level(cfg, seg):
     """The partial-free schedule on trees with several levels of sharing:
     rows fold segments of different levels into one accumulator, one launch
     per position along the path."""
-    print(f"[case] static config {cfg} schedule 4 seg={seg}", flush=True)
     wl = make_static(cfg)
+    print(f"[case] {wl.name} schedule 4 seg={seg}", flush=True)
     p = _static_pair(wl)
     p.cache.set_tuning(seg_chunks=seg, schedule=4)
     for rep in range(2):
         o, q, row_seq = p.attention({s.seq_id: wl.q[s.seq_id] for s in wl.seqs})
         ref = p.reference(row_seq, q, 0.0) if rep == 0 else ref
-        assert_close(o, ref, wl.dtype, f"config {cfg} schedule 4 seg={seg} rep={rep}")
+        assert_close(o, ref, wl.dtype, f"{wl.name} schedule 4 seg={seg} rep={rep}")
 
 
 @pytest.mark.timeout(900)
 def test_config5_dynamic_decode():
     """64 decode steps with churn: tables every step, sampled rows every step."""
-    print("[case] config 5 dynamic", flush=True)
+    print("[case] 64-step decode with churn, 128 rows", flush=True)
     wl = make_dynamic()
     p = Pair(wl.c, wl.H, wl.d, wl.dtype, 2600)
     seg_dev = {}
@@ -119,11 +119,11 @@ def test_config5_dynamic_decode():
         n_rows = len(row_seq) if st.step == 0 else (16 if st.step in (16, 63) else 3)
         rows = np.sort(rng.choice(len(row_seq), n_rows, replace=False))
         ref = p.reference(row_seq, q, 0.0, rows=list(rows))
-        ma, rel = assert_close(o[rows], ref, wl.dtype, f"config 5 step {st.step}")
+        ma, rel = assert_close(o[rows], ref, wl.dtype, f"decode step {st.step}")
         worst = (max(worst[0], ma), max(worst[1], rel))
         if st.step in (0, 17, 63):
             p.check_pool(max_nodes=32, rng=rng)
-    print(f"[parity] config 5 worst max_abs={worst[0]:.3e} rel_l2={worst[1]:.3e} "
+    print(f"[parity] 64-step decode worst max_abs={worst[0]:.3e} rel_l2={worst[1]:.3e} "
           f"uploads={p.cache.stats()['uploads'] - uploads_before}", flush=True)
 
 

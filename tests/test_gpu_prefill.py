@@ -16,7 +16,7 @@ def test_join_single_prompt_tree_512_new_tokens():
     """The prefill workload: a 33rd sequence joins the single-shared-prompt tree
     (1024 shared + 512 unique per row) with the shared prompt plus 512 new
     tokens; its 512 new tokens attend over 1536 positions."""
-    print("[case] prefill join config 2, 512 new tokens", flush=True)
+    print("[case] prefill join of the single-prompt tree, 512 new tokens", flush=True)
     pj = make_prefill_join()
     wl = pj.static
     p = Pair(wl.c, wl.H, wl.d, wl.dtype, 400)

@@ -131,7 +131,7 @@ def test_static_configs_bit_exact(cfg):
 
 
 def test_dynamic_config_replay_bit_exact():
-    """Config 5: 64 decode steps with churn; tables equal after every step."""
+    """64 decode steps with churn over 128 rows; tables equal after every step."""
     _lib_or_skip()
     wl = make_dynamic()
     h = B.ca_create(wl.c, wl.H, wl.d, B.CA_FP16, 1 << 16)

@@ -105,7 +105,7 @@ class DecodeStep:
 
 @dataclasses.dataclass
 class DynamicWorkload:
-    """Config 5: initial tree plus a generator of decode steps."""
+    """The 64-step decode workload: initial tree plus a generator of decode steps."""
 
     config: int
     name: str
@@ -208,7 +208,7 @@ def make_static(config: int) -> StaticWorkload:
             firsts.add(int(t[0]))
             seg_tokens.append(t)
             seqs.append(Sequence(i, [0, 1 + i]))
-    else:  # config 4: two roots, two branches under each, 16 suffixes per branch
+    else:  # two roots, two branches under each, 16 suffixes per branch
         roots = []
         rf = set()
         for _ in range(2):
@@ -248,7 +248,7 @@ def make_static(config: int) -> StaticWorkload:
 
 def make_dynamic(config: int = 5, n_steps: int = 64, B: int = 128,
                  prompt_len: int = 2048, H: int | None = None, d: int | None = None) -> DynamicWorkload:
-    """Config 5: shared prompt plus suffixes of U[64,1024] tokens, then decode.
+    """Shared prompt plus suffixes of U[64,1024] tokens, then decode.
 
     Churn: before steps 16, 32 and 48, round(0.1*B) live sequences chosen
     uniformly without replacement leave, and as many new ones (the same prompt
@@ -297,7 +297,8 @@ class PrefillJoin:
 
 def make_prefill_join(n_new: int = 512, config: int = 2) -> PrefillJoin:
     """The prefill-with-prefix-reuse workload: one more sequence joins the
-    single-shared-prompt tree (config 2 by default) with the 1024-token
+    single-shared-prompt tree (32 rows, 1024 shared + 512 unique tokens, by
+    default) with the 1024-token
     shared prompt plus ``n_new`` new tokens. Seeded with PCG64(1100 + config)
     after the static workload's own draws: new tokens (first token distinct
     from the existing branches), then K and V of the new tokens, then q."""
