@@ -206,15 +206,18 @@ def counter_traffic(workload):
     import hashlib
 
     path = os.path.join(ROOT, "profiles", "tpp_kernel_single_prompt_b32_traffic.json")
-    src = os.path.join(ROOT, "paper_2402_15220_amd", "csrc", "kernels.hip")
+    csrc = os.path.join(ROOT, "paper_2402_15220_amd", "csrc")
     try:
         with open(path) as f:
             rec = json.load(f)
-        with open(src, "rb") as f:
-            sha = hashlib.sha256(f.read()).hexdigest()[:16]
+        h = hashlib.sha256()
+        for name in ("kernels.hip", "device_common.hpp"):   # the decode kernels' sources
+            with open(os.path.join(csrc, name), "rb") as f:
+                h.update(f.read())
+        sha = h.hexdigest()[:16]
     except OSError:
         return None
-    if rec.get("kernels_hip_sha256_16") != sha or rec.get("workload") != workload:
+    if rec.get("decode_sources_sha256_16") != sha or rec.get("workload") != workload:
         return None
     return rec["kernels"]["tpp_kernel"]["traffic_bytes"]
 

@@ -1,0 +1,120 @@
+// Device helpers shared by the decode kernels (kernels.hip) and the prefill
+// kernel (prefill.hip), gfx950 only.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cfloat>
+#include <cstdint>
+
+namespace ca {
+namespace {
+
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef _Float16 half4 __attribute__((ext_vector_type(4)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+typedef __fp16 fp16x4_t __attribute__((__vector_size__(4 * sizeof(__fp16))));
+
+// ds_read_b64_tr_b16: each lane names 4 consecutive halves in LDS; within
+// every 16-lane group, lane i receives element i % 4 of the values named by
+// lanes 4j + i / 4, for j = 0..3. With lane (i, group g) naming row
+// r0 + 4g + i / 4, column c0 + 4 (i % 4) of a row-major [row][col] tile,
+// lane i gets rows r0 + 4g + j, column c0 + i: the 16x16x16 MFMA A operand
+// of the transposed tile, without a transposed copy.
+__device__ __forceinline__ half4 lds_read_tr16(const _Float16* p) {
+  const fp16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4f16(
+      (__attribute__((address_space(3))) fp16x4_t*)(p));
+  return __builtin_bit_cast(half4, v);
+}
+
+constexpr float kNegBig = -FLT_MAX;  // "no score yet": exp2(kNegBig - x) == 0, never NaN
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xF, 0xF, true));
+}
+
+// Sum over aligned groups of N lanes (N = 8, 16, 32 or 64); every lane of the
+// group receives the sum. Must be called with the whole wavefront active.
+template <int N>
+__device__ __forceinline__ float group_sum(float x) {
+  x += dpp<0xB1>(x);   // quad_perm [1,0,3,2]
+  x += dpp<0x4E>(x);   // quad_perm [2,3,0,1]
+  x += dpp<0x141>(x);  // row_half_mirror: groups of 8
+  if constexpr (N >= 16) x += dpp<0x140>(x);  // row_mirror: rows of 16
+  if constexpr (N >= 32) x += __shfl_xor(x, 16);
+  if constexpr (N >= 64) x += __shfl_xor(x, 32);
+  return x;
+}
+
+template <typename T>
+struct Elem;
+template <>
+struct Elem<_Float16> {
+  static constexpr int kPerVec = 8;  // elements per 16-byte vector
+  __device__ static __forceinline__ void unpack(const uint4& r, float* f) {
+    const half8 h = __builtin_bit_cast(half8, r);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) f[i] = static_cast<float>(h[i]);
+  }
+  __device__ static __forceinline__ uint4 pack(const float* f) {
+    half8 h;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) h[i] = static_cast<_Float16>(f[i]);
+    return __builtin_bit_cast(uint4, h);
+  }
+};
+template <>
+struct Elem<float> {
+  static constexpr int kPerVec = 4;
+  __device__ static __forceinline__ void unpack(const uint4& r, float* f) {
+    f[0] = __uint_as_float(r.x);
+    f[1] = __uint_as_float(r.y);
+    f[2] = __uint_as_float(r.z);
+    f[3] = __uint_as_float(r.w);
+  }
+  __device__ static __forceinline__ uint4 pack(const float* f) {
+    return make_uint4(__float_as_uint(f[0]), __float_as_uint(f[1]), __float_as_uint(f[2]),
+                      __float_as_uint(f[3]));
+  }
+};
+
+// attn_reduce (Eqn 2) in base 2: fold (mo, no, acco) into (m, n, acc).
+template <int E>
+__device__ __forceinline__ void fold(float& m, float& n, float* acc, float mo, float no,
+                                     const float* acco) {
+  const float mm = fmaxf(m, mo);
+  const float a = fast_exp2(m - mm);
+  const float b = fast_exp2(mo - mm);
+  n = n * a + no * b;
+#pragma unroll
+  for (int j = 0; j < E; ++j) acc[j] = acc[j] * a + acco[j] * b;
+  m = mm;
+}
+
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) x = fmaxf(x, __shfl_xor(x, off));
+  return x;
+}
+
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off);
+  return x;
+}
+
+__device__ __forceinline__ float readlane_f(float x, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), l));
+}
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// vmcnt(0): every vector memory access of this wavefront has completed
+__device__ __forceinline__ void wait_stores() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+}  // namespace
+}  // namespace ca

@@ -1,0 +1,434 @@
+// gfx950 (MI355X) prefill attention with prefix reuse over the prefix-tree,
+// chunked KV cache of ChunkAttention (arXiv 2402.15220, Section 3.2,
+// prefill paragraph).
+#include <hip/hip_runtime.h>
+
+#include <cfloat>
+#include <cstdint>
+
+#include "device_common.hpp"
+#include "kernels.hpp"
+
+namespace ca {
+namespace {
+
+// Prefill with prefix reuse (Section 3.2, prefill paragraph): once a joining
+// sequence's unmatched suffix has been written into the tree, its n_q
+// trailing tokens attend causally to the sequence's whole K/V, read chunk by
+// chunk along the root-to-leaf path. Query i sits at position
+// L - n_q + i and sees positions 0..L - n_q + i.
+//
+// One block per (64 queries, head), NGRP groups of WPG wavefronts. The
+// work is a list of units of TOK consecutive rows of one chunk (a chunk of
+// up to c tokens is ceil(c / TOK) units); group k takes units k, k+NGRP, ...
+// Each group has two LDS tiles: while it computes one unit from one tile,
+// the next unit is written into the other tile and the one after is loading
+// into registers, so one barrier per step suffices. Inside a group,
+// wavefront w owns QT = 4/WPG tiles of 16 queries and every token of the
+// group's units; K and V are staged as [token][d], once for all 64 queries,
+// and each K or V element read from LDS feeds QT matrix-core ops.
+//   S^T = K Q^T  (16x16x32 MFMA: K rows from LDS as A, the wavefront's q rows
+//                 as B, held in registers for the whole call);
+//   causal and chunk-length mask where a unit needs one, online softmax per
+//   query row (base 2, scale folded into the exponent);
+//   O^T += V^T P^T (16x16x32 MFMA: V^T read from LDS with the transposing
+//                 ds_read_b64_tr_b16 as A, P^T straight from the S^T
+//                 accumulators of two token tiles as B).
+// At the end the groups' states (m, n, O) are folded (Eqn 2) through LDS
+// and group 0 writes o = O / n.
+struct KpfParams {
+  const _Float16* q;            // [n_q][H][D]
+  _Float16* o;                  // [n_q][H][D]
+  const _Float16* kpool;
+  const _Float16* vpool;
+  int64_t ss, hs;               // pool strides of a slot and of a head (elements)
+  int n_chunks;                 // chunk_slot [n_chunks] path slots root -> leaf, chunk_start
+                                // [n_chunks + 1] first position of each chunk (last = L):
+                                // kernel arguments of their own
+  int n_q;
+  int H;
+  int C;
+  float qscale;                 // softmax scale * log2(e)
+};
+
+template <int D>
+constexpr int kpf_k_stride() { return D + 8; }   // halves per K (and V) row in LDS
+
+// TOK rows of a chunk's K and V (rows r0 .. r0 + TOK - 1) for a group of GT
+// threads: granule e = tid + GT*u is row r0 + e / (D/8), 16-byte column
+// e % (D/8) (coalesced rows). Rows past the chunk's length re-read its last
+// row (their scores are masked).
+template <int D, int GT, int TOK>
+__device__ __forceinline__ void kpf_load_rows(const _Float16* kbase, const _Float16* vbase,
+                                              size_t slot_stride, int slot, int r0, int len, int tid,
+                                              u32x4 (&kr)[TOK * D / 8 / GT],
+                                              u32x4 (&vr)[TOK * D / 8 / GT]) {
+  constexpr int NG = D / 8;
+  const _Float16* kb = kbase + slot * slot_stride;
+  const _Float16* vb = vbase + slot * slot_stride;
+#pragma unroll
+  for (int u = 0; u < TOK * NG / GT; ++u) {
+    const int e = tid + GT * u;
+    const size_t off = static_cast<size_t>(min(r0 + e / NG, len - 1)) * D + (e % NG) * 8;
+    kr[u] = *reinterpret_cast<const u32x4*>(kb + off);
+    vr[u] = *reinterpret_cast<const u32x4*>(vb + off);
+  }
+}
+
+template <int D, int TOK>
+constexpr int kpf_tile_bytes() { return 2 * TOK * kpf_k_stride<D>() * 2; }
+
+// A short path travels inside the kernel arguments (no upload before the
+// launch); NI is its capacity.
+template <int NI>
+struct KpfPath {
+  int32_t slot[NI];
+  int32_t start[NI + 1];
+};
+
+// Work unit: TOK consecutive rows of one chunk (a chunk of up to c tokens
+// has ceil(c / TOK) units). NI > 0: the path comes in `path` (at most NI
+// chunks); NI == 0: in the device arrays cslot / cstart.
+template <int D, int NGRP, int WPG, int TOK, int NI>
+__global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
+                                                              const int32_t* __restrict__ cslot,
+                                                              const int32_t* __restrict__ cstart,
+                                                              const KpfPath<(NI > 0 ? NI : 1)> path) {
+  constexpr int QT = 4 / WPG;       // 16-query tiles per wavefront
+  constexpr int GT = 64 * WPG;      // threads per group
+  constexpr int KS = D / 32;        // 16x16x32 steps over d
+  constexpr int DT = D / 16;        // 16-wide d tiles of O^T
+  constexpr int NG = D / 8;         // 16-byte granules per token row
+  constexpr int GPT = TOK * NG / GT;// granules of K (and of V) per thread per unit
+  constexpr int JT = TOK / 16;      // 16-token tiles of S^T per unit
+  constexpr int PV = TOK / 32;      // 32-token steps of O^T per unit
+  constexpr int KST = kpf_k_stride<D>();
+  constexpr int TB = kpf_tile_bytes<D, TOK>();
+  constexpr int OST = D + 4;         // merge buffer row stride (floats): rows start 4 banks apart
+  static_assert(WPG * QT == 4, "64 queries per block");
+  static_assert(TOK % 32 == 0 && TOK <= 64 && GPT * GT == TOK * NG, "unit shape");
+  static_assert(2 * TB * NGRP <= 160 * 1024, "two LDS tiles per group");
+  static_assert(NGRP == 1 || 2 * TB * NGRP >= (NGRP - 1) * 64 * (OST + 2) * 4, "merge buffer");
+  __shared__ __attribute__((aligned(16))) char lds[2 * TB * NGRP];
+  auto chunk_slot = [&](int j) -> int {
+    if constexpr (NI > 0) return path.slot[j];
+    else return cslot[j];
+  };
+  auto chunk_start = [&](int j) -> int {
+    if constexpr (NI > 0) return path.start[j];
+    else return cstart[j];
+  };
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int grp = __builtin_amdgcn_readfirstlane((tid >> 6) / WPG);  // uniform: unit indices stay scalar
+  const int w = (tid >> 6) % WPG;   // wavefront inside the group
+  const int gtid = tid % GT;        // thread index inside the group
+  const int l16 = lane & 15, g = lane >> 4;
+  // the group's two tiles: tile b holds K rows then V rows
+  auto tile_k = [&](int b) { return reinterpret_cast<_Float16*>(lds + (2 * grp + b) * TB); };
+  // XCD-aware tile order: blocks go to the eight XCDs round-robin, so block
+  // b runs on XCD b % 8; the tiles (head-major) are split into eight
+  // contiguous ranges, one per XCD, and every query tile of a head reads
+  // that head's chunks through the same L2.
+  const int H = P.H, n_q = P.n_q;
+  const int n_qt = (n_q + 63) / 64;
+  const int per_xcd = static_cast<int>(gridDim.x) / 8;
+  const int v = static_cast<int>(blockIdx.x % 8) * per_xcd + static_cast<int>(blockIdx.x / 8);
+  if (v >= n_qt * H) return;
+  const int h = v / n_qt;
+  const int L = chunk_start(P.n_chunks);
+  const int q0 = (v % n_qt) * 64;                              // first query of the tile
+  const int pos_last = L - n_q + min(q0 + 63, n_q - 1);        // last position of the tile
+  const int pos_first = L - n_q + q0;                          // first position of the tile
+  const size_t slot_stride = static_cast<size_t>(P.ss);
+  const _Float16* kbase = P.kpool + h * P.hs;
+  const _Float16* vbase = P.vpool + h * P.hs;
+  const int upc = (P.C + TOK - 1) / TOK;                       // units per chunk
+
+  // this lane's query row of tile t, and its position
+  int qi[QT], pos[QT];
+  half8 qf[QT][KS];
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    qi[t] = q0 + 16 * (QT * w + t) + l16;
+    pos[t] = L - n_q + qi[t];
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      if (qi[t] < n_q)
+        qf[t][s] = *reinterpret_cast<const half8*>(P.q + (static_cast<size_t>(qi[t]) * H + h) * D +
+                                                   32 * s + 8 * g);
+      else
+        qf[t][s] = half8{};
+    }
+  }
+  // q has arrived before any chunk load is issued, so the MFMAs inside the
+  // loop never wait on vector memory (the next unit's loads stay in flight)
+  wait_stores();
+  float m_run[QT], n_part[QT];
+  floatx4 acc[QT][DT];
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    m_run[t] = kNegBig;
+    n_part[t] = 0.f;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) acc[t][dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  // Chunks the tile needs: those starting at or before its last position
+  // (starts ascend); 64 starts per load, one per lane.
+  const int nc = P.n_chunks;
+  int n_ch = 0;
+  for (int b = 0; b < nc; b += 64) {
+    const int st = b + lane < nc ? chunk_start(b + lane) : 0x7fffffff;
+    const unsigned long long m = __ballot(st <= pos_last);
+    n_ch += __popcll(m);
+    if (m != ~0ull) break;
+  }
+  const int n_units = n_ch * upc;
+  // Per-chunk metadata comes through the scalar cache (uniform index,
+  // read-only arguments), so no metadata load ever waits behind the rows in
+  // flight. Past the end the registers reload the last unit: every step
+  // issues the same loads, so the wait before each LDS write covers exactly
+  // the registers it needs on every path.
+  u32x4 kr[GPT], vr[GPT];
+  auto issue = [&](int u) {
+    u = min(u, n_units - 1);
+    const int j = u / upc;
+    const int st = chunk_start(j);
+    kpf_load_rows<D, GT, TOK>(kbase, vbase, slot_stride, chunk_slot(j), TOK * (u % upc),
+                              chunk_start(j + 1) - st, gtid, kr, vr);
+  };
+  auto stage = [&](int b) {
+    _Float16* k_lds = tile_k(b);
+    _Float16* v_lds = k_lds + TOK * KST;
+#pragma unroll
+    for (int u = 0; u < GPT; ++u) {
+      const int e = gtid + GT * u;
+      *reinterpret_cast<u32x4*>(k_lds + (e / NG) * KST + (e % NG) * 8) = kr[u];
+      *reinterpret_cast<u32x4*>(v_lds + (e / NG) * KST + (e % NG) * 8) = vr[u];
+    }
+  };
+  auto compute = [&](int u, int b) {
+    const _Float16* k_lds = tile_k(b);
+    const _Float16* v_lds = k_lds + TOK * KST;
+    const int j = u / upc;
+    const int r0 = TOK * (u % upc);
+    const int c0 = chunk_start(j) + r0;                     // position of the unit's first row
+    const int len = min(TOK, chunk_start(j + 1) - c0);      // rows of the unit
+    if (len <= 0 || c0 > pos_last) return;                  // nothing the tile can see (uniform)
+
+    // S^T for the unit's token slots: tile jt holds tokens 16jt..16jt+15;
+    // each K read feeds the wavefront's QT query tiles. All of the unit's K
+    // fragments are read first (one wait), then the JT independent
+    // accumulation chains are interleaved on the matrix cores.
+    floatx4 sacc[QT][JT];
+    half8 ka[JT][KS];
+#pragma unroll
+    for (int jt = 0; jt < JT; ++jt)
+#pragma unroll
+      for (int s = 0; s < KS; ++s)
+        ka[jt][s] = *reinterpret_cast<const half8*>(k_lds + (16 * jt + l16) * KST + 32 * s + 8 * g);
+#pragma unroll
+    for (int jt = 0; jt < JT; ++jt)
+#pragma unroll
+      for (int t = 0; t < QT; ++t) sacc[t][jt] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < KS; ++s)
+#pragma unroll
+      for (int jt = 0; jt < JT; ++jt)
+#pragma unroll
+        for (int t = 0; t < QT; ++t)
+          sacc[t][jt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ka[jt][s], qf[t][s], sacc[t][jt], 0, 0, 0);
+    // lane holds S^T[token 16jt + 4g + i][row l16 of tile t] (unscaled).
+    // Units that are whole and end before the tile's first position need no
+    // mask (uniform test).
+    if (len < TOK || c0 + TOK - 1 > pos_first) {
+#pragma unroll
+      for (int t = 0; t < QT; ++t)
+#pragma unroll
+        for (int jt = 0; jt < JT; ++jt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int tk = 16 * jt + 4 * g + i;
+            if (!(tk < len && c0 + tk <= pos[t])) sacc[t][jt][i] = -INFINITY;
+          }
+    }
+    half8 pb[QT][PV];
+    bool moved = false;
+    float alpha[QT];
+#pragma unroll
+    for (int t = 0; t < QT; ++t) {
+      float lmax = -INFINITY;
+#pragma unroll
+      for (int jt = 0; jt < JT; ++jt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) lmax = fmaxf(lmax, sacc[t][jt][i]);
+      lmax = fmaxf(lmax, __shfl_xor(lmax, 16));
+      lmax = fmaxf(lmax, __shfl_xor(lmax, 32));
+      // running max in scaled base-2 units; qscale > 0 commutes with max
+      const float mn = fmaxf(m_run[t], lmax * P.qscale);
+      alpha[t] = fast_exp2(m_run[t] - mn);
+      moved |= alpha[t] != 1.f;
+      m_run[t] = mn;
+      half4 ph[JT];
+      float ps = 0.f;
+#pragma unroll
+      for (int jt = 0; jt < JT; ++jt) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float pv = fast_exp2(__builtin_fmaf(sacc[t][jt][i], P.qscale, -mn));
+          ph[jt][i] = static_cast<_Float16>(pv);
+          ps += pv;
+        }
+      }
+      n_part[t] = n_part[t] * alpha[t] + ps;
+      // O^T += V^T P^T over 32 tokens per 16x16x32 MFMA: lane group g's
+      // 8-token K-slice is tokens 4g..4g+3 of token tiles 2p and 2p+1 (any
+      // token order works as long as both operands share it), which is
+      // exactly what the lane holds of P^T; two transposing reads fetch the
+      // V^T side.
+#pragma unroll
+      for (int p2 = 0; p2 < PV; ++p2)
+        pb[t][p2] = __builtin_shufflevector(ph[2 * p2], ph[2 * p2 + 1], 0, 1, 2, 3, 4, 5, 6, 7);
+    }
+    // O is rescaled only when some row's maximum moved (uniform test)
+    if (__any(moved)) {
+#pragma unroll
+      for (int t = 0; t < QT; ++t)
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) acc[t][dt] *= alpha[t];
+    }
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+#pragma unroll
+      for (int p2 = 0; p2 < PV; ++p2) {
+        const _Float16* vp = v_lds + (32 * p2 + 4 * g + (l16 >> 2)) * KST + 16 * dt + 4 * (l16 & 3);
+        const half4 v0 = lds_read_tr16(vp);             // tokens 32p + 4g + j
+        const half4 v1 = lds_read_tr16(vp + 16 * KST);  // tokens 32p + 16 + 4g + j
+        const half8 va = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
+#pragma unroll
+        for (int t = 0; t < QT; ++t)
+          acc[t][dt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(va, pb[t][p2], acc[t][dt], 0, 0, 0);
+      }
+    }
+  };
+  // Two LDS tiles per group: step i computes the group's unit i from tile
+  // i % 2 while unit i + 1 is written into the other tile and unit i + 2
+  // loads into the registers; one barrier per step (after it, tile i % 2 is
+  // complete and nobody still reads the other one).
+  const int steps = (n_units + NGRP - 1) / NGRP;  // the same in every group
+  if (steps > 0) {
+    issue(grp);
+    stage(0);
+    issue(grp + NGRP);
+  }
+  for (int i = 0; i < steps; ++i) {
+    __syncthreads();
+    if (i + 1 < steps) {
+      stage((i + 1) & 1);
+      issue(grp + (i + 2) * NGRP);
+    }
+    const int u = grp + i * NGRP;
+    if (u < n_units) compute(u, i & 1);
+  }
+  // row sums over the four lane groups
+  float n_row[QT];
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    n_row[t] = n_part[t];
+    n_row[t] += __shfl_xor(n_row[t], 16);
+    n_row[t] += __shfl_xor(n_row[t], 32);
+  }
+  if constexpr (NGRP > 1) {
+    // groups 1.. hand their (m, n, O) to group 0 through LDS (Eqn 2)
+    float* ob = reinterpret_cast<float*>(lds);                    // [NGRP-1][64][OST]
+    float* mb = ob + (NGRP - 1) * 64 * OST;                        // [NGRP-1][64][2]
+    __syncthreads();  // the tiles are free
+    if (grp > 0) {
+#pragma unroll
+      for (int t = 0; t < QT; ++t) {
+        const int r = 16 * (QT * w + t) + l16;
+        float* o_ = ob + ((grp - 1) * 64 + r) * OST;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+          *reinterpret_cast<floatx4*>(o_ + 16 * dt + 4 * g) = acc[t][dt];
+        if (g == 0) {
+          mb[((grp - 1) * 64 + r) * 2] = m_run[t];
+          mb[((grp - 1) * 64 + r) * 2 + 1] = n_row[t];
+        }
+      }
+    }
+    __syncthreads();
+    if (grp > 0) return;
+#pragma unroll
+    for (int t = 0; t < QT; ++t) {
+      const int r = 16 * (QT * w + t) + l16;
+#pragma unroll
+      for (int k = 1; k < NGRP; ++k) {
+        const float mo = mb[((k - 1) * 64 + r) * 2], no = mb[((k - 1) * 64 + r) * 2 + 1];
+        const float M = fmaxf(m_run[t], mo);
+        const float ws = fast_exp2(m_run[t] - M), wo = fast_exp2(mo - M);
+        const float* o_ = ob + ((k - 1) * 64 + r) * OST;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+          acc[t][dt] = acc[t][dt] * ws + *reinterpret_cast<const floatx4*>(o_ + 16 * dt + 4 * g) * wo;
+        n_row[t] = n_row[t] * ws + no * wo;
+        m_run[t] = M;
+      }
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    if (qi[t] < n_q) {
+      const float inv = 1.f / n_row[t];
+      _Float16* out = P.o + (static_cast<size_t>(qi[t]) * H + h) * D;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        half4 r4;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) r4[i] = static_cast<_Float16>(acc[t][dt][i] * inv);
+        *reinterpret_cast<half4*>(out + 16 * dt + 4 * g) = r4;
+      }
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_prefill(const PrefillArgs& a, hipStream_t stream) {
+  if (a.n_q <= 0 || a.n_chunks <= 0) return hipSuccess;
+  KpfParams P{static_cast<const _Float16*>(a.q), static_cast<_Float16*>(a.o),
+              static_cast<const _Float16*>(a.kpool), static_cast<const _Float16*>(a.vpool), a.ss,
+              a.hs, a.n_chunks, a.n_q, a.H, a.C, a.qscale};
+  // two groups of four wavefronts (16 queries each), 64-row units, two LDS
+  // tiles per group
+  constexpr int kGroups = 2, kWaves = 4, kTok = 64;
+  const int tiles = ((a.n_q + 63) / 64) * a.H;
+  const dim3 grid(8 * ((tiles + 7) / 8));  // a multiple of the XCD count
+  const dim3 block(64 * kWaves * kGroups);
+  if (a.host_path && a.n_chunks <= kPrefillInlineChunks) {
+    KpfPath<kPrefillInlineChunks> path;
+    for (int j = 0; j < a.n_chunks; ++j) path.slot[j] = a.host_path[j];
+    for (int j = 0; j <= a.n_chunks; ++j) path.start[j] = a.host_path[a.n_chunks + j];
+    if (a.D == 128)
+      kpf_kernel<128, kGroups, kWaves, kTok, kPrefillInlineChunks><<<grid, block, 0, stream>>>(
+          P, nullptr, nullptr, path);
+    else if (a.D == 64)
+      kpf_kernel<64, kGroups, kWaves, kTok, kPrefillInlineChunks><<<grid, block, 0, stream>>>(
+          P, nullptr, nullptr, path);
+    else return hipErrorInvalidValue;
+    return hipGetLastError();
+  }
+  if (!a.chunk_slot) return hipErrorInvalidValue;
+  const KpfPath<1> none{};
+  if (a.D == 128)
+    kpf_kernel<128, kGroups, kWaves, kTok, 0><<<grid, block, 0, stream>>>(P, a.chunk_slot,
+                                                                         a.chunk_start, none);
+  else if (a.D == 64)
+    kpf_kernel<64, kGroups, kWaves, kTok, 0><<<grid, block, 0, stream>>>(P, a.chunk_slot,
+                                                                        a.chunk_start, none);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+}  // namespace ca
