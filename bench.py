@@ -63,7 +63,7 @@ def _parse():
 def main():
     args = _parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+        print("bench.py runs on one GPU only: the library has no multi-GPU path "
               "(heads would shard across GPUs with no collective in attention).", file=sys.stderr)
         sys.exit(2)
 
