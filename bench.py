@@ -362,6 +362,7 @@ def dynamic_run():
             for sid, toks, kk, vv in added:
                 cache.insert(sid, toks, kk, vv)
         cache.append(st.live, st.tokens, k, v)
+        cache.prepare()                 # the step's context, ahead of the q permutation
         order = cache.seq_order()
         n = len(order)
         pinned_idx[i, :n] = torch.from_numpy(np.searchsorted(st.live, order))

@@ -196,6 +196,19 @@ ca_status ca_workspace_size(const ca_cache* cache, size_t* bytes);
 ca_status ca_attention(ca_cache* cache, const void* q, void* o, float scale, void* ws,
                        size_t ws_bytes, void* stream);
 
+/* Bring the kernel context up to date now (Section 3.3, further
+ * optimizations: context generation hidden behind earlier GPU work). Builds
+ * the tables and work lists for the current tree on the host and, if they
+ * differ from the device copy, enqueues the upload on `stream`; a following
+ * ca_attention on the same stream then only launches kernels. Call it after
+ * a step's tree changes (joins, leaves, appends) and after enqueuing the GPU
+ * work that precedes attention, so the host work overlaps that work. Without
+ * it, ca_attention does the same lazily.
+ *   uploaded  nullable out: 1 if an upload was enqueued, else 0
+ * A table-only cache or an empty tree builds the host context only.
+ * Errors: INVALID (null cache), DEVICE. */
+ca_status ca_prepare(ca_cache* cache, void* stream, int32_t* uploaded);
+
 /* Prefill attention with prefix reuse (Section 3.2, prefill paragraph): a
  * joining sequence's matched prefix keeps its K/V in the tree, its unmatched
  * suffix is written by ca_insert/ca_extend, and attention then runs over the

@@ -102,6 +102,11 @@ class Cache:
     def set_tuning(self, seg_chunks=0, split_chunks=-1, phase_mask=0, schedule=-1):
         B.ca_set_tuning(self.h, seg_chunks, split_chunks, phase_mask, schedule)
 
+    def prepare(self) -> bool:
+        """Build the kernel context for the current tree now and enqueue its
+        upload on the current stream (True if one was needed)."""
+        return B.ca_prepare(self.h, None if self.table_only else self.stream())
+
     # -- attention ---------------------------------------------------------
     def workspace(self):
         need = B.ca_workspace_size(self.h)

@@ -544,6 +544,17 @@ ca_status ca_attention(ca_cache* cache, const void* q, void* o, float scale, voi
   return CA_OK;
 }
 
+ca_status ca_prepare(ca_cache* cache, void* stream, int32_t* uploaded) {
+  if (uploaded) *uploaded = 0;
+  if (!cache) return fail(CA_ERR_INVALID, "ca_prepare: null cache");
+  cache->ensure_work();
+  if (cache->table_only || cache->tree.num_seqs() == 0 || cache->dw_valid) return CA_OK;
+  ca_status st = cache->upload(static_cast<hipStream_t>(stream));
+  if (st != CA_OK) return st;
+  if (uploaded) *uploaded = 1;
+  return CA_OK;
+}
+
 ca_status ca_prefill_attention(ca_cache* cache, int64_t seq_id, const void* q, void* o,
                                int64_t n_q, float scale, void* stream) {
   if (!cache) return fail(CA_ERR_INVALID, "ca_prefill_attention: null cache");

@@ -354,3 +354,28 @@ def test_lazy_context_upload():
     o, qq, rs = p.attention(qmap())
     assert p.cache.stats()["uploads"] == u0 + 1
     assert_close(o, p.reference(rs, qq, 0.0), np.float16, "after chunk growth")
+
+
+def test_prepare_moves_the_context_upload():
+    """Section 3.3 (latency hiding): ca_prepare builds and uploads the context
+    ahead of the attention call, which then uploads nothing; a second prepare
+    with no tree change does nothing."""
+    rng = np.random.default_rng(5)
+    H, d = 2, 64
+    p = _small_pair(c=4, H=H, d=d)
+    k, v = _kv(rng, 6, H, d, np.float16)
+    p.insert(0, np.arange(6), k, v)
+    p.insert(1, np.concatenate([np.arange(4), [50, 51]]), k, v)
+    qmap = lambda: {s: rng.standard_normal((H, d)).astype(np.float16) for s in (0, 1)}  # noqa: E731
+    assert p.cache.prepare()
+    u0 = p.cache.stats()["uploads"]
+    assert not p.cache.prepare()
+    o, qq, rs = p.attention(qmap())
+    assert p.cache.stats()["uploads"] == u0
+    assert_close(o, p.reference(rs, qq, 0.0), np.float16, "after prepare")
+    for tok in (7, 8, 9):                               # the third append grows new chunks
+        p.append([0, 1], [tok, tok], *_kv(rng, 2, H, d, np.float16))
+    assert p.cache.prepare()
+    o, qq, rs = p.attention(qmap())
+    assert p.cache.stats()["uploads"] == u0 + 1
+    assert_close(o, p.reference(rs, qq, 0.0), np.float16, "after growth and prepare")

@@ -323,3 +323,15 @@ def test_partial_free_workspace_is_one_accumulator_per_row():
     assert B.ca_stats(h)["seg_chunks"] == 64
     assert B.ca_workspace_size(h) == ws4
     B.ca_destroy(h)
+
+
+def test_prepare_on_a_table_only_cache():
+    """ca_prepare builds the host context only (nothing to upload)."""
+    _lib_or_skip()
+    h = B.ca_create(4, 2, 64, B.CA_FP16, 64)
+    assert B.ca_prepare(h) is False                 # empty tree
+    B.ca_insert(h, 0, [1, 2, 3, 4, 5])
+    B.ca_insert(h, 1, [1, 2, 3, 4, 6])
+    assert B.ca_prepare(h) is False
+    assert B.ca_workspace_size(h) > 0
+    B.ca_destroy(h)
