@@ -173,21 +173,11 @@ def test_random_trees(seed):
             assert_close(o, ref, dtype, f"random tree seed={seed} op={i}")
 
 
-@pytest.mark.parametrize("c,dtype", [(128, np.float16), (100, np.float16), (65, np.float32),
-                                     (200, np.float16)])
-def test_random_trees_long_chunks(c, dtype):
-    """Chunks longer than the kernels' 64-token blocks: every chunk spans
-    several blocks, the last one ragged (c=100 under the partial-free
-    schedule)."""
-    seed = 40 + c
-    d, H = 128 if c % 2 == 0 else 64, 2
-    print(f"[case] long chunks c={c} dtype={np.dtype(dtype).name}", flush=True)
-    p = Pair(c, H, d, dtype, 1024)
-    if c == 100:  # the partial-free schedule, one segment per chunk
-        p.cache.set_tuning(seg_chunks=1, schedule=4)
+def _run_script(p, seed, ops, H, d, dtype, label, every=5):
+    """Apply a random operation script to the pair; check tables and parity
+    every `every` operations and after the last."""
     full = {}
     qrng = np.random.default_rng(2000 + seed)
-    ops = random_op_script(seed, n_ops=30, alphabet=3, max_len=2 * c + 40)
     for i, op in enumerate(ops):
         if op[0] == "insert":
             k, v = prefix_keyed_kv(seed, op[2], 0, H, d, dtype)
@@ -210,12 +200,47 @@ def test_random_trees_long_chunks(c, dtype):
         else:
             p.remove(op[1])
             del full[op[1]]
-        if full and (i % 5 == 4 or i == len(ops) - 1):
+        if full and (i % every == every - 1 or i == len(ops) - 1):
             p.check_tables()
             qmap = {sid: qrng.standard_normal((H, d)).astype(np.float32).astype(dtype) for sid in full}
             o, q, row_seq = p.attention(qmap)
             ref = p.reference(row_seq, q, 0.0)
-            assert_close(o, ref, dtype, f"long chunks c={c} op={i}")
+            assert_close(o, ref, dtype, f"{label} op={i}")
+
+
+@pytest.mark.parametrize("c,dtype", [(128, np.float16), (100, np.float16), (65, np.float32),
+                                     (200, np.float16)])
+def test_random_trees_long_chunks(c, dtype):
+    """Chunks longer than the kernels' 64-token blocks: every chunk spans
+    several blocks, the last one ragged (c=100 under the partial-free
+    schedule)."""
+    seed = 40 + c
+    d, H = 128 if c % 2 == 0 else 64, 2
+    print(f"[case] long chunks c={c} dtype={np.dtype(dtype).name}", flush=True)
+    p = Pair(c, H, d, dtype, 1024)
+    if c == 100:  # the partial-free schedule, one segment per chunk
+        p.cache.set_tuning(seg_chunks=1, schedule=4)
+    ops = random_op_script(seed, n_ops=30, alphabet=3, max_len=2 * c + 40)
+    _run_script(p, seed, ops, H, d, dtype, f"long chunks c={c}")
+
+
+@pytest.mark.parametrize("case", range(4))
+def test_random_trees_large(case):
+    """Larger trees: up to 48 live sequences of up to a few hundred tokens over
+    a 4-token alphabet (deep sharing, many splits and removals), 200
+    operations, under the default schedule with automatic segments, split
+    rows, and the partial-free schedule."""
+    seed = 300 + case
+    c = [8, 32, 16, 64][case]
+    H, d = 4, 128
+    tuning = [dict(), dict(split_chunks=2), dict(seg_chunks=2, schedule=4), dict(schedule=0)][case]
+    print(f"[case] large random tree c={c} tuning={tuning}", flush=True)
+    p = Pair(c, H, d, np.float16, 8192)
+    if tuning:
+        p.cache.set_tuning(**tuning)
+    ops = random_op_script(seed, n_ops=200, alphabet=4, max_len=80, max_live=48,
+                           p_insert=0.3, p_extend=0.25, p_append=0.3)
+    _run_script(p, seed, ops, H, d, np.float16, f"large tree c={c}", every=20)
 
 
 @pytest.mark.parametrize("sched", [0, 1, 2, 4])
