@@ -308,9 +308,10 @@ def dynamic_run():
     """The 64-step decode workload: every step appends one token to each live
     sequence (after churn on steps 16, 32, 48), then attends. Inputs of all
     steps are generated and copied to the GPU first; each step then times the
-    library calls only: attention alone with events, and the whole step
-    (remove/insert, append, row order, q permutation, attention) on the host
-    clock up to a synchronisation. A first, pipelined pass runs the same
+    library calls only: attention alone with events (q and o in the batch's
+    own order through the row map of ca_attention_ordered), and the whole step
+    (remove/insert, append, context preparation, attention) on the host clock
+    up to a synchronisation. A first, pipelined pass runs the same
     steps with no synchronisation in between and reports wall time per step
     against the GPU's busy span (host work hidden under device work)."""
     import numpy as np
@@ -349,7 +350,6 @@ def dynamic_run():
                           torch.from_numpy(st.q).cuda()))
     q_rows = torch.empty((256, wl.H, wl.d), dtype=torch.float16, device="cuda")
     o = torch.empty_like(q_rows)
-    pinned_idx = torch.empty((len(dev_steps), 256), dtype=torch.int64, pin_memory=True)
     torch.cuda.synchronize()
     t_gen = time.perf_counter() - t_gen
     st0 = cache.stats()
@@ -362,13 +362,8 @@ def dynamic_run():
             for sid, toks, kk, vv in added:
                 cache.insert(sid, toks, kk, vv)
         cache.append(st.live, st.tokens, k, v)
-        cache.prepare()                 # the step's context, ahead of the q permutation
-        order = cache.seq_order()
-        n = len(order)
-        pinned_idx[i, :n] = torch.from_numpy(np.searchsorted(st.live, order))
-        idx = pinned_idx[i, :n].cuda(non_blocking=True)
-        torch.index_select(q, 0, idx, out=q_rows[:n])
-        return n
+        cache.prepare()                 # the step's context, ahead of the launches
+        return len(st.live)
 
     # Pipelined pass: no synchronisation between steps, so the host work of a
     # step (tree update, context patch or rebuild and upload, launches) runs
@@ -376,15 +371,11 @@ def dynamic_run():
     # copy of the starting tree and leaves it as the timed pass expects.
     pipe = {}
     if len(dev_steps) > 0:
-        # one call on the starting tree first, with the same torch ops as a
-        # step: one-time costs (the library's device and pinned allocations,
-        # the first launch of torch's gather kernel, about 2 ms) stay out of
-        # the pipelined span
+        # one call on the starting tree first: one-time costs (the library's
+        # device and pinned allocations) stay out of the pipelined span
         q_rows.zero_()
-        n0 = len(cache.seq_order())
-        idx0 = torch.arange(n0, dtype=torch.int64).pin_memory().cuda(non_blocking=True)
-        torch.index_select(q_rows[:n0].clone(), 0, idx0, out=q_rows[:n0])
-        cache.attention(q_rows[:n0], out=o[:n0])
+        n0 = cache.num_seqs()
+        cache.attention(q_rows[:n0], out=o[:n0], seq_ids=cache.seq_order())
         torch.cuda.synchronize()
         ga = torch.cuda.Event(enable_timing=True)
         gb = torch.cuda.Event(enable_timing=True)
@@ -393,7 +384,7 @@ def dynamic_run():
         ga.record()
         for i, (st, added, k, v, q) in enumerate(dev_steps):
             n = one_step(i, st, added, k, v, q)
-            cache.attention(q_rows[:n], out=o[:n])
+            cache.attention(q, out=o[:n], seq_ids=st.live)   # q and o in the batch's own order
         gb.record()
         host_done = time.perf_counter()
         gb.synchronize()
@@ -419,7 +410,7 @@ def dynamic_run():
         t0 = time.perf_counter()
         n = one_step(i, st, added, k, v, q)
         a.record()
-        cache.attention(q_rows[:n], out=o[:n])
+        cache.attention(q, out=o[:n], seq_ids=st.live)
         b.record()
         b.synchronize()
         step_us.append((time.perf_counter() - t0) * 1e6)

@@ -196,6 +196,17 @@ ca_status ca_workspace_size(const ca_cache* cache, size_t* bytes);
 ca_status ca_attention(ca_cache* cache, const void* q, void* o, float scale, void* ws,
                        size_t ws_bytes, void* stream);
 
+/* ca_attention with q and o in the caller's row order: row i of q and o
+ * belongs to sequence seq_ids[i] (host, n entries), which must list every
+ * live sequence exactly once (n = ca_num_seqs). The kernels read q and write
+ * o through a tree-row -> caller-row map, so no gather of q or scatter of o
+ * is needed; the map is uploaded (library-owned pinned staging, on `stream`)
+ * only when it differs from the previous call's. Other arguments and
+ * errors as ca_attention, plus INVALID (n differs from the number of live
+ * sequences, an id not live or listed twice). */
+ca_status ca_attention_ordered(ca_cache* cache, const void* q, void* o, const int64_t* seq_ids,
+                               int64_t n, float scale, void* ws, size_t ws_bytes, void* stream);
+
 /* Bring the kernel context up to date now (Section 3.3, further
  * optimizations: context generation hidden behind earlier GPU work). Builds
  * the tables and work lists for the current tree on the host and, if they

@@ -114,8 +114,9 @@ class Cache:
             self._ws = torch.empty(max(need, 256), dtype=torch.uint8, device=self.k_pool.device)
         return self._ws, need
 
-    def attention(self, q, out=None, scale: float = 0.0):
-        """q: [B, H, d] in seq_order(); returns o of the same shape/dtype."""
+    def attention(self, q, out=None, scale: float = 0.0, seq_ids=None):
+        """q: [B, H, d] in seq_order(), or in the order of ``seq_ids`` (every
+        live sequence once) when given; returns o in the same row order."""
         if self.table_only:
             raise ValueError("table-only cache has no attention")
         Bn = self.num_seqs()
@@ -124,8 +125,12 @@ class Cache:
         if out is None:
             out = torch.empty_like(q)
         ws, need = self.workspace()
-        B.ca_attention(self.h, q.data_ptr(), out.data_ptr(), scale, ws.data_ptr(), ws.numel(),
-                       self.stream())
+        if seq_ids is None:
+            B.ca_attention(self.h, q.data_ptr(), out.data_ptr(), scale, ws.data_ptr(), ws.numel(),
+                           self.stream())
+        else:
+            B.ca_attention_ordered(self.h, q.data_ptr(), out.data_ptr(), seq_ids, scale,
+                                   ws.data_ptr(), ws.numel(), self.stream())
         return out
 
     def prefill(self, seq_id, q, out=None, scale: float = 0.0):

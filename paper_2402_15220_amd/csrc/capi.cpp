@@ -147,6 +147,10 @@ struct ca_cache {
   size_t d_cnt_cap = 0;
   PinnedStaging work_stage;     // kernel context uploads
   PinnedStaging prefill_stage;  // prefill paths
+  PinnedStaging rowmap_stage;   // caller row orders
+  int32_t* d_rowmap = nullptr;  // [B] tree row -> caller row, on the device
+  size_t d_rowmap_cap = 0;
+  std::vector<int32_t> rowmap;  // what d_rowmap holds (empty: nothing uploaded)
   char* d_path = nullptr;       // prefill path on the device (long paths)
   std::vector<int32_t> prefill_host_path;  // short paths, passed in the kernel arguments
   size_t d_path_cap = 0;
@@ -166,6 +170,7 @@ struct ca_cache {
     if (side.join) (void)hipEventDestroy(side.join);
     if (side.stream) (void)hipStreamDestroy(side.stream);
     if (d_path) (void)hipFree(d_path);
+    if (d_rowmap) (void)hipFree(d_rowmap);
   }
 
   size_t esize() const { return cfg.dtype == CA_FP16 ? 2 : 4; }
@@ -259,6 +264,34 @@ struct ca_cache {
     dw.n_seg_groups = W.seg_group_ptr.empty() ? 0 : static_cast<int32_t>(W.seg_group_ptr.size()) - 1;
     dw_valid = true;
     ++uploads;
+    return CA_OK;
+  }
+
+  // Tree row -> caller row for a caller order given as seq_ids[0..n) (every
+  // live sequence once); uploaded only when it differs from the device copy.
+  ca_status upload_row_map(const int64_t* seq_ids, int64_t n, hipStream_t stream) {
+    const size_t B = tables.row_seq.size();
+    std::vector<int32_t> map(B, -1);
+    for (int64_t i = 0; i < n; ++i) {
+      auto it = work.row_of_seq.find(seq_ids[i]);
+      if (it == work.row_of_seq.end())
+        return fail(CA_ERR_INVALID, "ca_attention_ordered: sequence " +
+                                        std::to_string(seq_ids[i]) + " is not live");
+      if (map[it->second] >= 0)
+        return fail(CA_ERR_INVALID, "ca_attention_ordered: sequence " +
+                                        std::to_string(seq_ids[i]) + " listed twice");
+      map[it->second] = static_cast<int32_t>(i);
+    }
+    if (map == rowmap) return CA_OK;
+    const size_t bytes = std::max<size_t>(B * sizeof(int32_t), 16);
+    ca_status st = ensure_device(reinterpret_cast<char**>(&d_rowmap), &d_rowmap_cap, bytes, stream,
+                                 "row map alloc");
+    if (st != CA_OK) return st;
+    char* h = nullptr;
+    if ((st = rowmap_stage.acquire(bytes, &h)) != CA_OK) return st;
+    std::memcpy(h, map.data(), B * sizeof(int32_t));
+    if ((st = rowmap_stage.copy(d_rowmap, bytes, stream)) != CA_OK) return st;
+    rowmap.swap(map);
     return CA_OK;
   }
 
@@ -486,10 +519,13 @@ ca_status ca_workspace_size(const ca_cache* cache, size_t* bytes) {
   return CA_OK;
 }
 
-ca_status ca_attention(ca_cache* cache, const void* q, void* o, float scale, void* ws,
-                       size_t ws_bytes, void* stream) {
+static ca_status attention_impl(ca_cache* cache, const void* q, void* o, float scale, void* ws,
+                                size_t ws_bytes, void* stream, const int64_t* seq_ids,
+                                int64_t n) {
   if (!cache) return fail(CA_ERR_INVALID, "ca_attention: null cache");
   if (cache->table_only) return fail(CA_ERR_INVALID, "ca_attention: table-only cache");
+  if (seq_ids && n != cache->tree.num_seqs())
+    return fail(CA_ERR_INVALID, "ca_attention_ordered: n differs from the number of live sequences");
   if (cache->tree.num_seqs() == 0) return CA_OK;
   if (!q || !o) return fail(CA_ERR_INVALID, "ca_attention: null q/o");
   if ((reinterpret_cast<uintptr_t>(q) | reinterpret_cast<uintptr_t>(o)) & 15)
@@ -504,6 +540,12 @@ ca_status ca_attention(ca_cache* cache, const void* q, void* o, float scale, voi
   if (!cache->dw_valid) {
     ca_status st = cache->upload(s);
     if (st != CA_OK) return st;
+  }
+  const int32_t* row_map = nullptr;
+  if (seq_ids) {
+    ca_status st = cache->upload_row_map(seq_ids, n, s);
+    if (st != CA_OK) return st;
+    row_map = cache->d_rowmap;
   }
   if (cache->schedule == 3) {
     ca_status st = cache->ensure_side();
@@ -539,9 +581,22 @@ ca_status ca_attention(ca_cache* cache, const void* q, void* o, float scale, voi
                : nullptr;
   a.qscale = sc * 1.4426950408889634f;
   a.cnt = cache->d_cnt;
+  a.row_map = row_map;
   hipError_t e = ca::launch_attention(a, cache->dw, s, cache->phase_mask, cache->side);
   if (e != hipSuccess) return hip_fail(e, "ca_attention launch");
   return CA_OK;
+}
+
+ca_status ca_attention(ca_cache* cache, const void* q, void* o, float scale, void* ws,
+                       size_t ws_bytes, void* stream) {
+  return attention_impl(cache, q, o, scale, ws, ws_bytes, stream, nullptr, 0);
+}
+
+ca_status ca_attention_ordered(ca_cache* cache, const void* q, void* o, const int64_t* seq_ids,
+                               int64_t n, float scale, void* ws, size_t ws_bytes, void* stream) {
+  if (!seq_ids && n > 0) return fail(CA_ERR_INVALID, "ca_attention_ordered: null seq_ids");
+  static const int64_t kNone = 0;
+  return attention_impl(cache, q, o, scale, ws, ws_bytes, stream, seq_ids ? seq_ids : &kNone, n);
 }
 
 ca_status ca_prepare(ca_cache* cache, void* stream, int32_t* uploaded) {

@@ -67,6 +67,12 @@ __device__ __forceinline__ void st_dev(float* p, float x) {
 __device__ __forceinline__ float ld_dev(const float* p) {
   return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+// Row of q and o that holds tree row `row`: the caller's order when a row
+// map is given, else tree order.
+__device__ __forceinline__ int io_row(const int32_t* row_map, int row) {
+  return row_map ? row_map[row] : row;
+}
+
 // Byte offset of element d of partial p, head h in the partial-O workspace.
 __device__ __forceinline__ uint32_t part_off(int p, int H, int D, int h, int d) {
   return ((static_cast<uint32_t>(p) * H + h) * D + d) * 4u;
@@ -165,14 +171,15 @@ __device__ __forceinline__ void fold_parts(int k0, int k1, const int32_t* parts,
 template <typename T, int D, bool DEV>
 __device__ __forceinline__ void finish_row(const int32_t* part_ptr, const int32_t* parts,
                                            const float* ws_o, uint32_t o_bytes, const float2* ws_ml,
-                                           void* o, int H, int row, int h, int lane) {
+                                           void* o, const int32_t* row_map, int H, int row,
+                                           int h, int lane) {
   const int d0 = (lane % (D / 4)) * 4;
   float m = kNegBig, n = 0.f, acc[4] = {0.f, 0.f, 0.f, 0.f};
   fold_parts<4, 256 / D, DEV>(part_ptr[row], part_ptr[row + 1], parts, ws_o, o_bytes, ws_ml, H, D,
                               h, d0, lane, m, n, acc);
   if (lane < D / 4) {
     const float inv = 1.f / n;
-    T* out = static_cast<T*>(o) + (static_cast<size_t>(row) * H + h) * D + d0;
+    T* out = static_cast<T*>(o) + (static_cast<size_t>(io_row(row_map, row)) * H + h) * D + d0;
 #pragma unroll
     for (int j = 0; j < 4; ++j) out[j] = static_cast<T>(acc[j] * inv);
   }
@@ -211,6 +218,7 @@ struct KsfParams {
   int C;
   float qscale;
   int32_t* cnt;  // partial-writing schedules: per (row, head) arrival counters, else null
+  const int32_t* row_map;  // tree row -> row of q and o (null: tree order)
 };
 
 // Lane layout: a token row of d elements is read by LPT = d/EPL lanes, 16
@@ -242,7 +250,7 @@ __device__ __forceinline__ void ksf_block(const KsfParams& P, int item, int h, c
   float qf[EPL];
   {
     const uint4 qr = *reinterpret_cast<const uint4*>(static_cast<const T*>(P.q) +
-                                                     (static_cast<size_t>(it.row) * H + h) * D +
+                                                     (static_cast<size_t>(io_row(P.row_map, it.row)) * H + h) * D +
                                                      sub * EPL);
     E::unpack(qr, qf);
   }
@@ -366,7 +374,7 @@ __device__ __forceinline__ void ksf_block(const KsfParams& P, int item, int h, c
     const float inv = 1.f / n;
 #pragma unroll
     for (int j = 0; j < EPL; ++j) acc[j] *= inv;
-    *reinterpret_cast<uint4*>(static_cast<T*>(P.o) + (static_cast<size_t>(it.row) * H + h) * D +
+    *reinterpret_cast<uint4*>(static_cast<T*>(P.o) + (static_cast<size_t>(io_row(P.row_map, it.row)) * H + h) * D +
                               sub * EPL) = E::pack(acc);
   } else {
     if (P.cnt) {
@@ -388,7 +396,7 @@ __device__ __forceinline__ void ksf_block(const KsfParams& P, int item, int h, c
         const float inv = 1.f / n;
 #pragma unroll
         for (int j = 0; j < EPL; ++j) acc[j] *= inv;
-        *reinterpret_cast<uint4*>(static_cast<T*>(P.o) + (static_cast<size_t>(it.row) * H + h) * D +
+        *reinterpret_cast<uint4*>(static_cast<T*>(P.o) + (static_cast<size_t>(io_row(P.row_map, it.row)) * H + h) * D +
                                   sub * EPL) = E::pack(acc);
         return;
       }
@@ -414,7 +422,7 @@ __device__ __forceinline__ void ksf_block(const KsfParams& P, int item, int h, c
         last = arrive_last(P.cnt + static_cast<size_t>(it.row) * H + h, need);
       }
       if (__shfl(last, 0))
-        finish_row<T, D, true>(P.part_ptr, P.parts, P.ws_o, P.o_bytes, P.ws_ml, P.o, H, it.row, h,
+        finish_row<T, D, true>(P.part_ptr, P.parts, P.ws_o, P.o_bytes, P.ws_ml, P.o, P.row_map, H, it.row, h,
                                lane);
     }
   }
@@ -425,6 +433,7 @@ __device__ __forceinline__ void ksf_block(const KsfParams& P, int item, int h, c
 
 struct KmgParams {
   void* o;
+  const int32_t* row_map;
   const int32_t* mg_rows;
   const int32_t* part_ptr;
   const int32_t* parts;
@@ -436,7 +445,7 @@ struct KmgParams {
 
 template <typename T, int D>
 __global__ __launch_bounds__(64) void kmg_kernel(KmgParams P) {
-  finish_row<T, D, false>(P.part_ptr, P.parts, P.ws_o, P.o_bytes, P.ws_ml, P.o, P.H,
+  finish_row<T, D, false>(P.part_ptr, P.parts, P.ws_o, P.o_bytes, P.ws_ml, P.o, P.row_map, P.H,
                           P.mg_rows[blockIdx.x],
                           blockIdx.y, threadIdx.x);
 }
@@ -464,6 +473,7 @@ struct KcfParams {
   void* o;
   const int32_t* part_ptr;
   const int32_t* parts;
+  const int32_t* row_map;  // tree row -> row of q and o (null: tree order)
 };
 
 // Partial-writing schedules: after a chunk-first block wrote its partials for rows
@@ -491,7 +501,7 @@ __device__ __forceinline__ void cf_arrive(const KcfParams& P, int rb, int nrows,
   if (!any) return;
   for (int r = w; r < nrows; r += 4)
     if (flags[r])
-      finish_row<T, D, true>(P.part_ptr, P.parts, P.ws_o, P.o_bytes, P.ws_ml, P.o, P.H, rb + r,
+      finish_row<T, D, true>(P.part_ptr, P.parts, P.ws_o, P.o_bytes, P.ws_ml, P.o, P.row_map, P.H, rb + r,
                              h, lane);
 }
 
@@ -565,7 +575,7 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
       if (r < nrows)
-        qf[t][s] = *reinterpret_cast<const half8*>(q + (static_cast<size_t>(rb + r) * H + h) * D +
+        qf[t][s] = *reinterpret_cast<const half8*>(q + (static_cast<size_t>(io_row(P.row_map, rb + r)) * H + h) * D +
                                                    32 * s + 8 * g);
       else
         qf[t][s] = half8{};
@@ -876,7 +886,7 @@ __device__ __forceinline__ void kcf_f32_block(const KcfParams& P, int seg, int z
         for (int t = 0; t < NRT; ++t) {
           if (t < nrt) {
             const int r = 16 * t + l16;
-            const float b = r < nrows ? q[(static_cast<size_t>(rb + r) * H + h) * D + 4 * s + g] : 0.f;
+            const float b = r < nrows ? q[(static_cast<size_t>(io_row(P.row_map, rb + r)) * H + h) * D + 4 * s + g] : 0.f;
             sacc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, sacc[t], 0, 0, 0);
           }
         }
@@ -1150,10 +1160,10 @@ hipError_t launch_all(const AttnArgs& a, const DevWork& w, hipStream_t s, int ma
   const bool counting = w.schedule == 2 || w.schedule == 3;  // the last contributor finishes each row
   P.cf = KcfParams{a.q, a.kpool, a.vpool, a.ss, a.hs, a.slot_len, w.segs, w.seg_slots, a.ws_o,
                    reinterpret_cast<float2*>(a.ws_ml), a.ws_o_bytes, a.H, a.C, a.qscale,
-                   counting ? a.cnt : nullptr, a.o, w.part_ptr, w.parts};
+                   counting ? a.cnt : nullptr, a.o, w.part_ptr, w.parts, a.row_map};
   P.sf = KsfParams{a.q, a.o, a.kpool, a.vpool, a.ss, a.hs, a.slot_len, w.items, w.priv_slot, w.part_ptr,
                    w.parts, a.ws_o, reinterpret_cast<float2*>(a.ws_ml), a.ws_o_bytes, a.H, a.C,
-                   a.qscale, counting ? a.cnt : nullptr};
+                   a.qscale, counting ? a.cnt : nullptr, a.row_map};
   // At most 16 or 32 covered rows per chunk-first block; wider runs take
   // several row blocks, which re-read the chunk. Their block indices differ
   // by a multiple of H, so for H a multiple of 8 they land on the same XCD
@@ -1175,7 +1185,7 @@ hipError_t launch_all(const AttnArgs& a, const DevWork& w, hipStream_t s, int ma
   // epilogue runs in the sequential schedule (split rows) or on its own.
   const bool self_finished = counting && (mask & 3) == 3;
   if ((mask & 4) && w.n_mg > 0 && !self_finished) {
-    KmgParams M{a.o, w.mg_rows, w.part_ptr, w.parts, a.ws_o, reinterpret_cast<const float2*>(a.ws_ml),
+    KmgParams M{a.o, a.row_map, w.mg_rows, w.part_ptr, w.parts, a.ws_o, reinterpret_cast<const float2*>(a.ws_ml),
                 a.ws_o_bytes, a.H};
     kmg_kernel<T, D><<<dim3(w.n_mg, a.H), 64, 0, s>>>(M);
   }

@@ -52,6 +52,7 @@ struct AttnArgs {
   uint32_t ws_o_bytes;  // bytes of the ws_o region (below 4 GiB)
   float qscale;  // softmax scale * log2(e)
   int32_t* cnt;  // [B][H] arrival counters, zero between launches
+  const int32_t* row_map = nullptr;  // [B] tree row -> row of q and o (null: tree order)
 };
 
 // Enqueue the attention kernels. `phase_mask` selects phases (bit 0

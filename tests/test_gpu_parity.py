@@ -404,3 +404,65 @@ def test_prepare_moves_the_context_upload():
     o, qq, rs = p.attention(qmap())
     assert p.cache.stats()["uploads"] == u0 + 1
     assert_close(o, p.reference(rs, qq, 0.0), np.float16, "after growth and prepare")
+
+
+@pytest.mark.parametrize("sched", [2, 0, 4])
+def test_attention_in_caller_order(sched):
+    """ca_attention_ordered: q and o in an arbitrary order of the live
+    sequences give the same rows as the tree-order call; the order may change
+    between calls and the tree may change under a fixed order (joins, leaves,
+    growth); bad orders are refused."""
+    print(f"[case] caller order schedule={sched}", flush=True)
+    rng = np.random.default_rng(11 + sched)
+    H, d, c = 2, 64, 4
+    p = Pair(c, H, d, np.float16, 1024)
+    p.cache.set_tuning(schedule=sched)
+    base = rng.integers(0, 20, 30).astype(np.int32)
+    full = {}
+    for sid in range(12):
+        toks = np.concatenate([base[:int(rng.integers(1, 30))], rng.integers(20, 40, int(rng.integers(1, 20)))]).astype(np.int32)
+        k, v = prefix_keyed_kv(11, toks, 0, H, d, np.float16)
+        p.insert(sid, toks, k, v)
+        full[sid] = toks
+
+    def check(order, label):
+        qh = {s: rng.standard_normal((H, d)).astype(np.float16) for s in order}
+        q = to_dev(np.stack([qh[s] for s in order]))
+        o = p.cache.attention(q, seq_ids=np.asarray(order, np.int64))
+        torch.cuda.synchronize()
+        row_seq = p.cache.seq_order()
+        qt = np.stack([qh[int(s)] for s in row_seq])
+        ref = p.reference(row_seq, qt, 0.0)
+        pos = {int(s): i for i, s in enumerate(row_seq)}
+        assert_close(o.cpu().numpy(), ref[[pos[s] for s in order]], np.float16, label)
+
+    live = list(full)
+    for rep in range(3):
+        order = [int(x) for x in rng.permutation(live)]
+        check(order, f"order {rep}")
+    # the tree changes under a fixed caller order: a leave, a join, growth
+    p.remove(live[3])
+    live.remove(live[3])
+    toks = np.concatenate([base[:5], [99, 98, 97]]).astype(np.int32)
+    k, v = prefix_keyed_kv(11, toks, 0, H, d, np.float16)
+    p.insert(50, toks, k, v)
+    full[50] = toks
+    live.append(50)
+    ks, vs = [], []
+    for s in live:
+        t2 = np.concatenate([full[s], [7]]).astype(np.int32)
+        k, v = prefix_keyed_kv(11, t2, len(full[s]), H, d, np.float16)
+        ks.append(k)
+        vs.append(v)
+        full[s] = t2
+    p.append(live, [7] * len(live), np.concatenate(ks), np.concatenate(vs))
+    order = sorted(live, reverse=True)
+    check(order, "after tree changes")
+    q = to_dev(np.zeros((len(live), H, d), np.float16))
+    o = torch.empty_like(q)
+    ws, _ = p.cache.workspace()
+    for bad in (order[:-1], order[:-1] + [order[0]], order[:-1] + [12345]):
+        with pytest.raises(B.ChunkAttnError) as ei:
+            B.ca_attention_ordered(p.cache.h, q.data_ptr(), o.data_ptr(), np.asarray(bad, np.int64),
+                                   0.0, ws.data_ptr(), ws.numel(), p.cache.stream())
+        assert ei.value.status == B.CA_ERR_INVALID
