@@ -52,6 +52,8 @@ def _parse():
     ap.add_argument("--no-cold", action="store_true", help="skip the cache-evicted timing")
     ap.add_argument("--no-dynamic", action="store_true", help="skip the 64-step decode workload")
     ap.add_argument("--no-prefill", action="store_true", help="skip the prefill-with-prefix-reuse timing")
+    ap.add_argument("--dynamic-only", action="store_true",
+                    help="run only the 64-step decode workload and print its figures (for profiling it)")
     ap.add_argument("--seg", type=int, default=0, help="chunk-first segment size (0: library default)")
     ap.add_argument("--split", type=int, default=-1, help="sequence-first split (-1: library default)")
     ap.add_argument("--schedule", type=int, default=-1,
@@ -66,6 +68,9 @@ def main():
         print("bench.py runs on one GPU only: the library has no multi-GPU path "
               "(heads would shard across GPUs with no collective in attention).", file=sys.stderr)
         sys.exit(2)
+    if args.dynamic_only:
+        print(json.dumps({"dynamic": dynamic_run()}), flush=True)
+        return
 
     import numpy as np
     import torch
