@@ -203,6 +203,23 @@ def main():
     print(json.dumps(out), flush=True)
 
 
+def decode_sources_hash(csrc):
+    """Hash of the decode kernels' code (kernels.hip and device_common.hpp)
+    with comments and blank space removed, so that only code changes make
+    committed counter results stale."""
+    import hashlib
+    import re
+
+    h = hashlib.sha256()
+    for name in ("kernels.hip", "device_common.hpp"):
+        with open(os.path.join(csrc, name)) as f:
+            src = f.read()
+        src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+        src = re.sub(r"//[^\n]*", " ", src)
+        h.update(" ".join(src.split()).encode())
+    return h.hexdigest()[:16]
+
+
 def counter_traffic(workload):
     """HBM bytes per tpp_kernel launch from the committed rocprofv3 counter
     passes (FETCH_SIZE and WRITE_SIZE scaled by a plain copy), or None when
@@ -215,11 +232,7 @@ def counter_traffic(workload):
     try:
         with open(path) as f:
             rec = json.load(f)
-        h = hashlib.sha256()
-        for name in ("kernels.hip", "device_common.hpp"):   # the decode kernels' sources
-            with open(os.path.join(csrc, name), "rb") as f:
-                h.update(f.read())
-        sha = h.hexdigest()[:16]
+        sha = decode_sources_hash(csrc)
     except OSError:
         return None
     if rec.get("decode_sources_sha256_16") != sha or rec.get("workload") != workload:

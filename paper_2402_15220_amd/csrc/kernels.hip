@@ -2,30 +2,35 @@
 // KV cache with the two-phase partition of ChunkAttention (arXiv 2402.15220,
 // Section 3.2).
 //
-// Pools: K and V, each [slot][head][c][d]; slot_len[slot] holds the number of
-// valid rows of every slot. q and o: [B][H][d] in tree row order.
-// Softmax runs in base 2: scores are multiplied by scale*log2(e), so partial
-// maxima stored in the workspace are in log2 units.
+// Pools: K and V tiles of c x d elements per (slot, head) at slot and head
+// strides; slot_len[slot] holds the number of valid rows of every slot.
+// q and o: [B][H][d], in tree row order or, through a row map, in the
+// caller's order. Softmax runs in base 2: scores are multiplied by
+// scale*log2(e), so partial maxima stored in the workspace are in log2 units.
 //
-// Two schedules: the phases as consecutive launches, or both in ONE launch
-// (tpp_kernel) whose first blocks are chunk-first items and the rest
-// sequence-first items, so the latency-bound chunk-first work overlaps the
-// bandwidth-bound stream.
+// Schedules (ca_set_tuning): the phases as consecutive launches (0); both in
+// ONE launch (tpp_kernel) whose first blocks are chunk-first items and the
+// rest sequence-first items, so the latency-bound chunk-first work overlaps
+// the bandwidth-bound stream, with a merge launch (1) or with the last
+// contributor of each row merging inside the launch (2, default); the phases
+// on two streams (3); and the partial-free serial reduction (4), one
+// chunk-first launch per position along the rows' paths.
 //   kcf  chunk-first phase (Algorithm 1, Eqn 1). One workgroup per (segment
 //        of shared chunks, head, block of <= 16*NRT covered rows). For every
 //        64-token block of a chunk it forms S^T = K Q^T on the matrix cores
 //        (the covered query rows batched as the N dimension), updates the
 //        online softmax per row, and accumulates O^T = V^T P^T, again on the
-//        matrix cores. It writes one unnormalised partial (O, m, n) per row.
+//        matrix cores. It writes one unnormalised partial (O, m, n) per row
+//        (or, in schedule 4, folds it into the row's accumulator).
 //   ksf  sequence-first phase (Algorithm 2). One workgroup per (row, head,
 //        piece of the row's private chunks): a bandwidth-bound pass with
 //        16-byte loads, sub-wavefront DPP reductions for q.k and per-lane
 //        online softmax. An item that owns its row folds the row's
-//        chunk-first partials (sequential schedule) and writes O/n; otherwise
-//        it writes a partial.
+//        chunk-first partials and writes O/n; otherwise it writes a partial.
 //   kmg  merge epilogue (Algorithm 2's attn_reduce over the partials, Eqn 2,
 //        then O/n) for every row that has partials.
 //   kkv  K/V row copies for tree operations (new chunks, split tails).
+// The prefill kernel lives in prefill.hip.
 #include <hip/hip_runtime.h>
 
 #include <cfloat>
