@@ -52,7 +52,9 @@ struct KpfParams {
 };
 
 template <int D>
-constexpr int kpf_k_stride() { return D + 8; }   // halves per K (and V) row in LDS
+constexpr int kpf_k_stride() { return D + 8; }
+template <int D>
+constexpr int kpf_v_stride() { return D + 16; }
 
 // TOK rows of a chunk's K and V (rows r0 .. r0 + TOK - 1) for a group of GT
 // threads: granule e = tid + GT*u is row r0 + e / (D/8), 16-byte column
@@ -75,8 +77,35 @@ __device__ __forceinline__ void kpf_load_rows(const _Float16* kbase, const _Floa
   }
 }
 
+// Reductions over the four 16-lane rows of a wavefront (lanes l, l^16, l^32,
+// l^48) with gfx950's row-swap moves instead of LDS permutes. Swapping a
+// register with a copy of itself, odd rows against even rows, leaves rows
+// 2k and 2k+1 of the value in the two registers of every lane of both rows;
+// the half swap does the same for the two 32-lane halves. The s_nop covers
+// the wait states the swap needs after a vector write of its operands.
+__device__ __forceinline__ void kpf_swap_rows(float& a, float& b) {
+  asm volatile("s_nop 1\n\tv_permlane16_swap_b32 %0, %1" : "+v"(a), "+v"(b));
+}
+__device__ __forceinline__ void kpf_swap_halves(float& a, float& b) {
+  asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1" : "+v"(a), "+v"(b));
+}
+__device__ __forceinline__ float kpf_rows_max(float x) {
+  float a = x, b = x;
+  kpf_swap_rows(a, b);
+  float c = fmaxf(a, b), d = c;
+  kpf_swap_halves(c, d);
+  return fmaxf(c, d);
+}
+__device__ __forceinline__ float kpf_rows_sum(float x) {
+  float a = x, b = x;
+  kpf_swap_rows(a, b);
+  float c = a + b, d = c;
+  kpf_swap_halves(c, d);
+  return c + d;
+}
+
 template <int D, int TOK>
-constexpr int kpf_tile_bytes() { return 2 * TOK * kpf_k_stride<D>() * 2; }
+constexpr int kpf_tile_bytes() { return TOK * (kpf_k_stride<D>() + kpf_v_stride<D>()) * 2; }
 
 // A short path travels inside the kernel arguments (no upload before the
 // launch); NI is its capacity.
@@ -103,6 +132,7 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
   constexpr int JT = TOK / 16;      // 16-token tiles of S^T per unit
   constexpr int PV = TOK / 32;      // 32-token steps of O^T per unit
   constexpr int KST = kpf_k_stride<D>();
+  constexpr int VST = kpf_v_stride<D>();
   constexpr int TB = kpf_tile_bytes<D, TOK>();
   constexpr int OST = D + 4;         // merge buffer row stride (floats): rows start 4 banks apart
   static_assert(WPG * QT == 4, "64 queries per block");
@@ -110,13 +140,35 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
   static_assert(2 * TB * NGRP <= 160 * 1024, "two LDS tiles per group");
   static_assert(NGRP == 1 || 2 * TB * NGRP >= (NGRP - 1) * 64 * (OST + 2) * 4, "merge buffer");
   __shared__ __attribute__((aligned(16))) char lds[2 * TB * NGRP];
+  // Chunk j's slot, first position and end. A path of up to 64 chunks keeps
+  // chunk j's three values in lane j and reads them with v_readlane, so the
+  // unit loop has no memory wait for them (a scalar load's wait would also
+  // drain the wavefront's LDS operations); longer paths read the kernel
+  // arguments or the device arrays through the scalar cache.
+  constexpr bool kLane = NI > 0 && NI <= 64;
+  int lane_slot = 0, lane_start = 0x7fffffff, lane_end = 0;
+  if constexpr (kLane) {
+    const int l = threadIdx.x & 63;
+    if (l < P.n_chunks) {
+      lane_slot = path.slot[l];
+      lane_start = path.start[l];
+      lane_end = path.start[l + 1];
+    }
+  }
   auto chunk_slot = [&](int j) -> int {
-    if constexpr (NI > 0) return path.slot[j];
+    if constexpr (kLane) return __builtin_amdgcn_readlane(lane_slot, j);
+    else if constexpr (NI > 0) return path.slot[j];
     else return cslot[j];
   };
   auto chunk_start = [&](int j) -> int {
-    if constexpr (NI > 0) return path.start[j];
+    if constexpr (kLane) return __builtin_amdgcn_readlane(lane_start, j);
+    else if constexpr (NI > 0) return path.start[j];
     else return cstart[j];
+  };
+  auto chunk_end = [&](int j) -> int {
+    if constexpr (kLane) return __builtin_amdgcn_readlane(lane_end, j);
+    else if constexpr (NI > 0) return path.start[j + 1];
+    else return cstart[j + 1];
   };
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -136,7 +188,7 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
   const int v = static_cast<int>(blockIdx.x % 8) * per_xcd + static_cast<int>(blockIdx.x / 8);
   if (v >= n_qt * H) return;
   const int h = v / n_qt;
-  const int L = chunk_start(P.n_chunks);
+  const int L = chunk_end(P.n_chunks - 1);
   const int q0 = (v % n_qt) * 64;                              // first query of the tile
   const int pos_last = L - n_q + min(q0 + 63, n_q - 1);        // last position of the tile
   const int pos_first = L - n_q + q0;                          // first position of the tile
@@ -178,25 +230,37 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
   // (starts ascend); 64 starts per load, one per lane.
   const int nc = P.n_chunks;
   int n_ch = 0;
-  for (int b = 0; b < nc; b += 64) {
-    const int st = b + lane < nc ? chunk_start(b + lane) : 0x7fffffff;
-    const unsigned long long m = __ballot(st <= pos_last);
-    n_ch += __popcll(m);
-    if (m != ~0ull) break;
+  if constexpr (kLane) {
+    n_ch = __popcll(__ballot(lane_start <= pos_last));
+  } else {
+    for (int b = 0; b < nc; b += 64) {
+      const int st = b + lane < nc ? chunk_start(b + lane) : 0x7fffffff;
+      const unsigned long long m = __ballot(st <= pos_last);
+      n_ch += __popcll(m);
+      if (m != ~0ull) break;
+    }
   }
   const int n_units = n_ch * upc;
-  // Per-chunk metadata comes through the scalar cache (uniform index,
-  // read-only arguments), so no metadata load ever waits behind the rows in
-  // flight. Past the end the registers reload the last unit: every step
-  // issues the same loads, so the wait before each LDS write covers exactly
-  // the registers it needs on every path.
+  // unit u is rows r0 .. r0 + TOK - 1 of chunk j (no division when every
+  // chunk is one unit; uniform)
+  auto unit_pos = [&](int u, int& j, int& r0) {
+    if (upc == 1) {
+      j = u;
+      r0 = 0;
+    } else {
+      j = u / upc;
+      r0 = TOK * (u - j * upc);
+    }
+  };
+  // Past the end the registers reload the last unit: every step issues the
+  // same loads, so the wait before each LDS write covers exactly the
+  // registers it needs on every path.
   u32x4 kr[GPT], vr[GPT];
   auto issue = [&](int u) {
-    u = min(u, n_units - 1);
-    const int j = u / upc;
-    const int st = chunk_start(j);
-    kpf_load_rows<D, GT, TOK>(kbase, vbase, slot_stride, chunk_slot(j), TOK * (u % upc),
-                              chunk_start(j + 1) - st, gtid, kr, vr);
+    int j, r0;
+    unit_pos(min(u, n_units - 1), j, r0);
+    kpf_load_rows<D, GT, TOK>(kbase, vbase, slot_stride, chunk_slot(j), r0,
+                              chunk_end(j) - chunk_start(j), gtid, kr, vr);
   };
   auto stage = [&](int b) {
     _Float16* k_lds = tile_k(b);
@@ -205,16 +269,16 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
     for (int u = 0; u < GPT; ++u) {
       const int e = gtid + GT * u;
       *reinterpret_cast<u32x4*>(k_lds + (e / NG) * KST + (e % NG) * 8) = kr[u];
-      *reinterpret_cast<u32x4*>(v_lds + (e / NG) * KST + (e % NG) * 8) = vr[u];
+      *reinterpret_cast<u32x4*>(v_lds + (e / NG) * VST + (e % NG) * 8) = vr[u];
     }
   };
   auto compute = [&](int u, int b) {
     const _Float16* k_lds = tile_k(b);
     const _Float16* v_lds = k_lds + TOK * KST;
-    const int j = u / upc;
-    const int r0 = TOK * (u % upc);
+    int j, r0;
+    unit_pos(u, j, r0);
     const int c0 = chunk_start(j) + r0;                     // position of the unit's first row
-    const int len = min(TOK, chunk_start(j + 1) - c0);      // rows of the unit
+    const int len = min(TOK, chunk_end(j) - c0);            // rows of the unit
     if (len <= 0 || c0 > pos_last) return;                  // nothing the tile can see (uniform)
 
     // S^T for the unit's token slots: tile jt holds tokens 16jt..16jt+15;
@@ -263,8 +327,7 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
       for (int jt = 0; jt < JT; ++jt)
 #pragma unroll
         for (int i = 0; i < 4; ++i) lmax = fmaxf(lmax, sacc[t][jt][i]);
-      lmax = fmaxf(lmax, __shfl_xor(lmax, 16));
-      lmax = fmaxf(lmax, __shfl_xor(lmax, 32));
+      lmax = kpf_rows_max(lmax);
       // running max in scaled base-2 units; qscale > 0 commutes with max
       const float mn = fmaxf(m_run[t], lmax * P.qscale);
       alpha[t] = fast_exp2(m_run[t] - mn);
@@ -302,9 +365,9 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
     for (int dt = 0; dt < DT; ++dt) {
 #pragma unroll
       for (int p2 = 0; p2 < PV; ++p2) {
-        const _Float16* vp = v_lds + (32 * p2 + 4 * g + (l16 >> 2)) * KST + 16 * dt + 4 * (l16 & 3);
+        const _Float16* vp = v_lds + (32 * p2 + 4 * g + (l16 >> 2)) * VST + 16 * dt + 4 * (l16 & 3);
         const half4 v0 = lds_read_tr16(vp);             // tokens 32p + 4g + j
-        const half4 v1 = lds_read_tr16(vp + 16 * KST);  // tokens 32p + 16 + 4g + j
+        const half4 v1 = lds_read_tr16(vp + 16 * VST);  // tokens 32p + 16 + 4g + j
         const half8 va = __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7);
 #pragma unroll
         for (int t = 0; t < QT; ++t)
@@ -335,9 +398,7 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
   float n_row[QT];
 #pragma unroll
   for (int t = 0; t < QT; ++t) {
-    n_row[t] = n_part[t];
-    n_row[t] += __shfl_xor(n_row[t], 16);
-    n_row[t] += __shfl_xor(n_row[t], 32);
+    n_row[t] = kpf_rows_sum(n_part[t]);
   }
   if constexpr (NGRP > 1) {
     // groups 1.. hand their (m, n, O) to group 0 through LDS (Eqn 2)
@@ -403,9 +464,24 @@ hipError_t launch_prefill(const PrefillArgs& a, hipStream_t stream) {
   // two groups of four wavefronts (16 queries each), 64-row units, two LDS
   // tiles per group
   constexpr int kGroups = 2, kWaves = 4, kTok = 64;
+  // paths up to this long keep their chunk table in the lanes of a register
+  constexpr int kLaneChunks = 64;
   const int tiles = ((a.n_q + 63) / 64) * a.H;
   const dim3 grid(8 * ((tiles + 7) / 8));  // a multiple of the XCD count
   const dim3 block(64 * kWaves * kGroups);
+  if (a.host_path && a.n_chunks <= kLaneChunks) {
+    KpfPath<kLaneChunks> path;
+    for (int j = 0; j < a.n_chunks; ++j) path.slot[j] = a.host_path[j];
+    for (int j = 0; j <= a.n_chunks; ++j) path.start[j] = a.host_path[a.n_chunks + j];
+    if (a.D == 128)
+      kpf_kernel<128, kGroups, kWaves, kTok, kLaneChunks><<<grid, block, 0, stream>>>(
+          P, nullptr, nullptr, path);
+    else if (a.D == 64)
+      kpf_kernel<64, kGroups, kWaves, kTok, kLaneChunks><<<grid, block, 0, stream>>>(
+          P, nullptr, nullptr, path);
+    else return hipErrorInvalidValue;
+    return hipGetLastError();
+  }
   if (a.host_path && a.n_chunks <= kPrefillInlineChunks) {
     KpfPath<kPrefillInlineChunks> path;
     for (int j = 0; j < a.n_chunks; ++j) path.slot[j] = a.host_path[j];
