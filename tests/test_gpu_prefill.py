@@ -94,11 +94,12 @@ def test_prefill_errors_and_noop():
         p32.cache.prefill(0, to_dev(np.zeros((3, 2, 64), np.float32)))
 
 
-@pytest.mark.parametrize("c,L", [(1, 255), (1, 256), (2, 700)])
+@pytest.mark.parametrize("c,L", [(16, 1024), (16, 1025), (3, 192), (1, 255), (1, 256), (2, 700)])
 def test_prefill_long_paths(c, L):
-    """Paths of up to 255 chunks travel in the kernel arguments, longer ones
-    through a device upload: both sides of that limit, and a long path of
-    short chunks."""
+    """Paths of up to 64 chunks keep their chunk table in register lanes, up
+    to 255 travel in the kernel arguments, longer ones through a device
+    upload: both sides of each limit (64 and 65, 255 and 256 chunks), and
+    long paths of short chunks."""
     print(f"[case] prefill path of {-(-L // c)} chunks (c={c}, L={L})", flush=True)
     H, d = 2, 64
     rng = np.random.default_rng(900 + L)
