@@ -18,9 +18,15 @@
  *     are already cached so their K/V need not be recomputed.
  *
  * Conventions for every call:
- *   - Return value: CA_OK (0) or a negative ca_status. On failure nothing
- *     observable changes (tree, tables, pool contents and slot ownership stay
- *     as they were) and ca_last_error() returns a message for this thread.
+ *   - Return value: CA_OK (0) or a negative ca_status, and ca_last_error()
+ *     returns a message for this thread. On failure nothing observable
+ *     changes (tree, tables, pool contents and slot ownership stay as they
+ *     were), with two exceptions: after CA_ERR_HOST the cache's host state
+ *     may be partly updated and the cache must be destroyed; after
+ *     CA_ERR_DEVICE from ca_insert, ca_extend or ca_append_batch the tree
+ *     change is kept but its K/V copies may not have been enqueued (HIP
+ *     launch errors are normally sticky, so the cache should be destroyed
+ *     too). No C++ exception leaves the library.
  *   - A cache is not thread-safe. All device work of a cache is enqueued on
  *     the hipStream_t passed to the call; callers must use one stream per
  *     cache, which also makes slot reuse after ca_remove safe (later writes
@@ -52,7 +58,8 @@ typedef enum {
   CA_ERR_NOT_FOUND = -3, /* unknown sequence id */
   CA_ERR_EXISTS = -4,    /* sequence id already live */
   CA_ERR_DEVICE = -5,    /* a HIP call failed; message holds hipGetErrorString */
-  CA_ERR_WORKSPACE = -6  /* workspace null or smaller than ca_workspace_size */
+  CA_ERR_WORKSPACE = -6, /* workspace null or smaller than ca_workspace_size */
+  CA_ERR_HOST = -7       /* a host memory allocation inside the library failed */
 } ca_status;
 
 typedef enum { CA_FP16 = 0, CA_FP32 = 1 } ca_dtype;

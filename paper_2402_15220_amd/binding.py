@@ -22,8 +22,9 @@ CA_ERR_NOT_FOUND = -3
 CA_ERR_EXISTS = -4
 CA_ERR_DEVICE = -5
 CA_ERR_WORKSPACE = -6
+CA_ERR_HOST = -7
 STATUS_NAMES = {0: "OK", -1: "INVALID", -2: "NOMEM", -3: "NOT_FOUND", -4: "EXISTS",
-                -5: "DEVICE", -6: "WORKSPACE"}
+                -5: "DEVICE", -6: "WORKSPACE", -7: "HOST"}
 
 CA_FP16 = 0
 CA_FP32 = 1

@@ -28,7 +28,7 @@ COMMON = [
     "-Wall", "-Wno-unused-result", f"-I{INCLUDE}", f"-I{CSRC}",
 ]
 
-SOURCES = ["tree.cpp", "tables.cpp", "capi.cpp", "kernels.hip", "prefill.hip"]
+SOURCES = ["tree.cpp", "tables.cpp", "capi.cpp", "kernels.hip", "prefill.hip", "fill.hip"]
 
 
 def _compile(src: str, objdir: str) -> str:

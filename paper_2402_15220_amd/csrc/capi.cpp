@@ -45,6 +45,27 @@ ca_status hip_fail(hipError_t e, const char* what) {
   return fail(CA_ERR_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
 }
 
+// Called from the catch clause of an entry point: no C++ exception crosses
+// the C ABI. Host allocations (tree, tables, work lists, messages) are the
+// only source of exceptions in the library.
+ca_status on_exception(const char* what) noexcept {
+  auto note = [what](const char* tail) noexcept {
+    try {
+      g_err.assign(what).append(tail);
+    } catch (...) {
+      g_err.clear();  // no memory even for the message
+    }
+  };
+  try {
+    throw;
+  } catch (const std::bad_alloc&) {
+    note(": out of host memory");
+  } catch (...) {
+    note(": unexpected internal error");
+  }
+  return CA_ERR_HOST;
+}
+
 int env_int(const char* name, int dflt) {
   const char* s = std::getenv(name);
   return s && *s ? std::atoi(s) : dflt;
@@ -323,7 +344,7 @@ struct ca_cache {
     const size_t cap = std::max<size_t>(n * 2, 1024);
     if ((e = hipMalloc(reinterpret_cast<void**>(&d_cnt), cap * sizeof(int32_t))) != hipSuccess)
       return hip_fail(e, "counter alloc");
-    if ((e = hipMemsetAsync(d_cnt, 0, cap * sizeof(int32_t), stream)) != hipSuccess)
+    if ((e = ca::launch_fill_i32(d_cnt, static_cast<int64_t>(cap), 0, stream)) != hipSuccess)
       return hip_fail(e, "counter clear");
     d_cnt_cap = cap;
     return CA_OK;
@@ -366,7 +387,7 @@ extern "C" {
 
 const char* ca_last_error(void) { return g_err.c_str(); }
 
-ca_status ca_create(const ca_config* cfg, ca_cache** out) {
+ca_status ca_create(const ca_config* cfg, ca_cache** out) try {
   if (!cfg || !out) return fail(CA_ERR_INVALID, "ca_create: null argument");
   if (cfg->chunk_size < 1) return fail(CA_ERR_INVALID, "ca_create: chunk_size < 1");
   if (cfg->num_heads < 1) return fail(CA_ERR_INVALID, "ca_create: num_heads < 1");
@@ -392,7 +413,7 @@ ca_status ca_create(const ca_config* cfg, ca_cache** out) {
       return fail(CA_ERR_INVALID, "ca_create: strides must be multiples of 16 bytes");
   }
   ca_cache* c = new (std::nothrow) ca_cache(norm);
-  if (!c) return fail(CA_ERR_INVALID, "ca_create: out of host memory");
+  if (!c) return fail(CA_ERR_HOST, "ca_create: out of host memory");
   c->table_only = cfg->k_pool == nullptr;
   c->seg_chunks = std::max(0, env_int("CA_CF_SEG", 0));
   c->split_chunks = env_int("CA_SPLIT", 0);
@@ -414,6 +435,8 @@ ca_status ca_create(const ca_config* cfg, ca_cache** out) {
   }
   *out = c;
   return CA_OK;
+} catch (...) {
+  return on_exception("ca_create");
 }
 
 ca_status ca_destroy(ca_cache* cache) {
@@ -439,16 +462,18 @@ static ca_status check_kv(const ca_cache* c, const void* k, const void* v, const
   return CA_OK;
 }
 
-ca_status ca_match(const ca_cache* cache, const int32_t* tokens, int64_t n, int64_t* matched) {
+ca_status ca_match(const ca_cache* cache, const int32_t* tokens, int64_t n, int64_t* matched) try {
   if (!cache || !matched) return fail(CA_ERR_INVALID, "ca_match: null argument");
   ca_status s = check_tokens(tokens, n, "ca_match");
   if (s != CA_OK) return s;
   *matched = cache->tree.match(tokens, n);
   return CA_OK;
+} catch (...) {
+  return on_exception("ca_match");
 }
 
 ca_status ca_insert(ca_cache* cache, int64_t seq_id, const int32_t* tokens, int64_t n,
-                    const void* k, const void* v, void* stream, int64_t* matched) {
+                    const void* k, const void* v, void* stream, int64_t* matched) try {
   if (!cache) return fail(CA_ERR_INVALID, "ca_insert: null cache");
   ca_status s = check_tokens(tokens, n, "ca_insert");
   if (s != CA_OK) return s;
@@ -459,10 +484,12 @@ ca_status ca_insert(ca_cache* cache, int64_t seq_id, const int32_t* tokens, int6
   if (e != ca::Err::ok) return from_err(e, "ca_insert");
   if (matched) *matched = m;
   return cache->run_jobs(jobs, k, v, static_cast<hipStream_t>(stream));
+} catch (...) {
+  return on_exception("ca_insert");
 }
 
 ca_status ca_extend(ca_cache* cache, int64_t seq_id, const int32_t* tokens, int64_t n,
-                    const void* k, const void* v, void* stream, int64_t* matched) {
+                    const void* k, const void* v, void* stream, int64_t* matched) try {
   if (!cache) return fail(CA_ERR_INVALID, "ca_extend: null cache");
   ca_status s = check_tokens(tokens, n, "ca_extend");
   if (s != CA_OK) return s;
@@ -473,10 +500,12 @@ ca_status ca_extend(ca_cache* cache, int64_t seq_id, const int32_t* tokens, int6
   if (e != ca::Err::ok) return from_err(e, "ca_extend");
   if (matched) *matched = m;
   return cache->run_jobs(jobs, k, v, static_cast<hipStream_t>(stream));
+} catch (...) {
+  return on_exception("ca_extend");
 }
 
 ca_status ca_append_batch(ca_cache* cache, int64_t n_seqs, const int64_t* seq_ids,
-                          const int32_t* tokens, const void* k, const void* v, void* stream) {
+                          const int32_t* tokens, const void* k, const void* v, void* stream) try {
   if (!cache) return fail(CA_ERR_INVALID, "ca_append_batch: null cache");
   if (n_seqs < 0 || n_seqs > INT32_MAX) return fail(CA_ERR_INVALID, "ca_append_batch: bad n_seqs");
   if (n_seqs == 0) return CA_OK;
@@ -488,11 +517,15 @@ ca_status ca_append_batch(ca_cache* cache, int64_t n_seqs, const int64_t* seq_id
   ca::Err e = cache->tree.append_batch(n_seqs, seq_ids, tokens, &jobs);
   if (e != ca::Err::ok) return from_err(e, "ca_append_batch");
   return cache->run_jobs(jobs, k, v, static_cast<hipStream_t>(stream));
+} catch (...) {
+  return on_exception("ca_append_batch");
 }
 
-ca_status ca_remove(ca_cache* cache, int64_t seq_id) {
+ca_status ca_remove(ca_cache* cache, int64_t seq_id) try {
   if (!cache) return fail(CA_ERR_INVALID, "ca_remove: null cache");
   return from_err(cache->tree.remove(seq_id), "ca_remove");
+} catch (...) {
+  return on_exception("ca_remove");
 }
 
 ca_status ca_num_seqs(const ca_cache* cache, int64_t* B) {
@@ -501,7 +534,7 @@ ca_status ca_num_seqs(const ca_cache* cache, int64_t* B) {
   return CA_OK;
 }
 
-ca_status ca_seq_order(const ca_cache* cache, int64_t* seq_ids, int64_t cap) {
+ca_status ca_seq_order(const ca_cache* cache, int64_t* seq_ids, int64_t cap) try {
   if (!cache || (!seq_ids && cache->tree.num_seqs() > 0))
     return fail(CA_ERR_INVALID, "ca_seq_order: null argument");
   if (cap < cache->tree.num_seqs()) return fail(CA_ERR_INVALID, "ca_seq_order: cap < B");
@@ -509,14 +542,18 @@ ca_status ca_seq_order(const ca_cache* cache, int64_t* seq_ids, int64_t cap) {
   c->ensure_work();
   std::copy(c->tables.row_seq.begin(), c->tables.row_seq.end(), seq_ids);
   return CA_OK;
+} catch (...) {
+  return on_exception("ca_seq_order");
 }
 
-ca_status ca_workspace_size(const ca_cache* cache, size_t* bytes) {
+ca_status ca_workspace_size(const ca_cache* cache, size_t* bytes) try {
   if (!cache || !bytes) return fail(CA_ERR_INVALID, "ca_workspace_size: null argument");
   ca_cache* c = const_cast<ca_cache*>(cache);
   c->ensure_work();
   *bytes = c->ws_bytes();
   return CA_OK;
+} catch (...) {
+  return on_exception("ca_workspace_size");
 }
 
 static ca_status attention_impl(ca_cache* cache, const void* q, void* o, float scale, void* ws,
@@ -588,18 +625,22 @@ static ca_status attention_impl(ca_cache* cache, const void* q, void* o, float s
 }
 
 ca_status ca_attention(ca_cache* cache, const void* q, void* o, float scale, void* ws,
-                       size_t ws_bytes, void* stream) {
+                       size_t ws_bytes, void* stream) try {
   return attention_impl(cache, q, o, scale, ws, ws_bytes, stream, nullptr, 0);
+} catch (...) {
+  return on_exception("ca_attention");
 }
 
 ca_status ca_attention_ordered(ca_cache* cache, const void* q, void* o, const int64_t* seq_ids,
-                               int64_t n, float scale, void* ws, size_t ws_bytes, void* stream) {
+                               int64_t n, float scale, void* ws, size_t ws_bytes, void* stream) try {
   if (!seq_ids && n > 0) return fail(CA_ERR_INVALID, "ca_attention_ordered: null seq_ids");
   static const int64_t kNone = 0;
   return attention_impl(cache, q, o, scale, ws, ws_bytes, stream, seq_ids ? seq_ids : &kNone, n);
+} catch (...) {
+  return on_exception("ca_attention_ordered");
 }
 
-ca_status ca_prepare(ca_cache* cache, void* stream, int32_t* uploaded) {
+ca_status ca_prepare(ca_cache* cache, void* stream, int32_t* uploaded) try {
   if (uploaded) *uploaded = 0;
   if (!cache) return fail(CA_ERR_INVALID, "ca_prepare: null cache");
   cache->ensure_work();
@@ -608,10 +649,12 @@ ca_status ca_prepare(ca_cache* cache, void* stream, int32_t* uploaded) {
   if (st != CA_OK) return st;
   if (uploaded) *uploaded = 1;
   return CA_OK;
+} catch (...) {
+  return on_exception("ca_prepare");
 }
 
 ca_status ca_prefill_attention(ca_cache* cache, int64_t seq_id, const void* q, void* o,
-                               int64_t n_q, float scale, void* stream) {
+                               int64_t n_q, float scale, void* stream) try {
   if (!cache) return fail(CA_ERR_INVALID, "ca_prefill_attention: null cache");
   if (cache->table_only) return fail(CA_ERR_INVALID, "ca_prefill_attention: table-only cache");
   if (cache->cfg.dtype != CA_FP16)
@@ -689,9 +732,11 @@ ca_status ca_prefill_attention(ca_cache* cache, int64_t seq_id, const void* q, v
   hipError_t e = ca::launch_prefill(a, s);
   if (e != hipSuccess) return hip_fail(e, "ca_prefill_attention launch");
   return CA_OK;
+} catch (...) {
+  return on_exception("ca_prefill_attention");
 }
 
-ca_status ca_export_tables(const ca_cache* cache, ca_tables* out) {
+ca_status ca_export_tables(const ca_cache* cache, ca_tables* out) try {
   if (!cache || !out) return fail(CA_ERR_INVALID, "ca_export_tables: null argument");
   ca_cache* c = const_cast<ca_cache*>(cache);
   ca::build_tables(c->tree, &c->exported);
@@ -713,6 +758,8 @@ ca_status ca_export_tables(const ca_cache* cache, ca_tables* out) {
   out->shr_ptr = T.shr_ptr.data();
   out->shr_part = T.shr_part.data();
   return CA_OK;
+} catch (...) {
+  return on_exception("ca_export_tables");
 }
 
 ca_status ca_set_tuning(ca_cache* cache, int32_t seg_chunks, int32_t split_chunks,
@@ -743,7 +790,7 @@ ca_status ca_set_tuning(ca_cache* cache, int32_t seg_chunks, int32_t split_chunk
 
 ca_status ca_stats(const ca_cache* cache, int64_t* uploads, int64_t* slots_used,
                    int64_t* slots_total, int32_t* schedule, int32_t* seg_chunks,
-                   int64_t* patches) {
+                   int64_t* patches) try {
   if (!cache) return fail(CA_ERR_INVALID, "ca_stats: null cache");
   if (!cache->patch_error.empty()) return fail(CA_ERR_INVALID, cache->patch_error);
   if (patches) *patches = cache->patches;
@@ -757,6 +804,8 @@ ca_status ca_stats(const ca_cache* cache, int64_t* uploads, int64_t* slots_used,
     *seg_chunks = c->work.seg_chunks;
   }
   return CA_OK;
+} catch (...) {
+  return on_exception("ca_stats");
 }
 
 }  // extern "C"

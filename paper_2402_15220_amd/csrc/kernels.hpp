@@ -82,6 +82,9 @@ struct PrefillArgs {
 };
 hipError_t launch_prefill(const PrefillArgs& a, hipStream_t stream);
 
+// p[0 .. n) = value on `stream` (a kernel, not a memset node).
+hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t value, hipStream_t stream);
+
 // K/V row copies for tree operations (at most kKvJobsPerLaunch per call).
 constexpr int kKvJobsPerLaunch = 64;
 hipError_t launch_kv_jobs(const KvJob* jobs, int n, int dtype, int H, int D, int C, int64_t ss,

@@ -335,3 +335,32 @@ def test_prepare_on_a_table_only_cache():
     assert B.ca_prepare(h) is False
     assert B.ca_workspace_size(h) > 0
     B.ca_destroy(h)
+
+
+def test_host_allocation_failure_is_a_status():
+    """A host allocation failure inside the library comes back as CA_ERR_HOST
+    with a message instead of an exception crossing the C ABI: a child
+    process caps its address space 128 MiB above what it uses, then inserts
+    a 10^8-token sequence into a table-only cache (the tree's chunks need
+    ~400 MB)."""
+    import subprocess
+    import sys
+    _lib_or_skip()
+    script = (
+        "import resource, sys\n"
+        "import numpy as np\n"
+        f"sys.path.insert(0, {ROOT!r})\n"
+        "from paper_2402_15220_amd import binding as B\n"
+        "h = B.ca_create(1024, 2, 64, B.CA_FP16, 1 << 20)\n"
+        "toks = (np.arange(100_000_000, dtype=np.int64) % 50000).astype(np.int32)\n"
+        "vm = int(open('/proc/self/statm').read().split()[0]) * resource.getpagesize()\n"
+        "resource.setrlimit(resource.RLIMIT_AS, (vm + (128 << 20), resource.getrlimit(resource.RLIMIT_AS)[1]))\n"
+        "try:\n"
+        "    B.ca_insert(h, 1, toks)\n"
+        "    print('inserted')\n"
+        "except B.ChunkAttnError as e:\n"
+        "    print('status', e.status, str(e))\n")
+    r = subprocess.run([sys.executable, "-c", script], capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0, r.stderr[-2000:]
+    assert f"status {B.CA_ERR_HOST}" in r.stdout, r.stdout + r.stderr[-2000:]
+    assert "out of host memory" in r.stdout
