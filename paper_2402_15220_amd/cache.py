@@ -60,10 +60,21 @@ class Cache:
                 raise ValueError("table-only cache takes no K/V")
             return None, None, None
         for t in (k, v):
-            if t.dtype != self.dtype or not t.is_cuda or tuple(t.shape) != (n, self.H, self.d) \
-                    or not t.is_contiguous():
-                raise ValueError(f"K/V must be contiguous {self.dtype} [{n},{self.H},{self.d}] on the GPU")
+            if not isinstance(t, torch.Tensor) or t.dtype != self.dtype \
+                    or tuple(t.shape) != (n, self.H, self.d) or not t.is_contiguous() \
+                    or t.device != self.k_pool.device:
+                raise ValueError(f"K/V must be contiguous {self.dtype} tensors [{n},{self.H},{self.d}] "
+                                 f"on {self.k_pool.device}")
         return k.data_ptr(), v.data_ptr(), self.stream()
+
+    def _check_rows(self, t, n, name):
+        """q and o: contiguous [n, H, d] of the cache's dtype on the pools'
+        device (the kernels read and write exactly n*H*d elements)."""
+        if not isinstance(t, torch.Tensor) or t.dtype != self.dtype or t.dim() != 3 \
+                or tuple(t.shape) != (n, self.H, self.d) or not t.is_contiguous() \
+                or t.device != self.k_pool.device:
+            raise ValueError(f"{name} must be a contiguous {self.dtype} tensor [{n},{self.H},{self.d}] "
+                             f"on {self.k_pool.device}")
 
     # -- tree operations ---------------------------------------------------
     def match(self, tokens) -> int:
@@ -120,10 +131,10 @@ class Cache:
         if self.table_only:
             raise ValueError("table-only cache has no attention")
         Bn = self.num_seqs()
-        if q.dtype != self.dtype or tuple(q.shape) != (Bn, self.H, self.d) or not q.is_contiguous():
-            raise ValueError(f"q must be contiguous {self.dtype} [{Bn},{self.H},{self.d}]")
+        self._check_rows(q, Bn, "q")
         if out is None:
             out = torch.empty_like(q)
+        self._check_rows(out, Bn, "out")
         ws, need = self.workspace()
         if seq_ids is None:
             B.ca_attention(self.h, q.data_ptr(), out.data_ptr(), scale, ws.data_ptr(), ws.numel(),
@@ -138,11 +149,12 @@ class Cache:
         its whole K/V (prefill after a prefix-matched insert). q: [n_q, H, d]."""
         if self.table_only:
             raise ValueError("table-only cache has no attention")
-        if q.dtype != self.dtype or q.dim() != 3 or tuple(q.shape[1:]) != (self.H, self.d) \
-                or not q.is_contiguous() or not q.is_cuda:
-            raise ValueError(f"q must be contiguous {self.dtype} [n_q,{self.H},{self.d}] on the GPU")
+        if not isinstance(q, torch.Tensor) or q.dim() != 3:
+            raise ValueError(f"q must be a tensor [n_q,{self.H},{self.d}]")
+        self._check_rows(q, q.shape[0], "q")
         if out is None:
             out = torch.empty_like(q)
+        self._check_rows(out, q.shape[0], "out")
         B.ca_prefill_attention(self.h, seq_id, q.data_ptr(), out.data_ptr(), q.shape[0], scale,
                                self.stream())
         return out

@@ -466,3 +466,39 @@ def test_attention_in_caller_order(sched):
             B.ca_attention_ordered(p.cache.h, q.data_ptr(), o.data_ptr(), np.asarray(bad, np.int64),
                                    0.0, ws.data_ptr(), ws.numel(), p.cache.stream())
         assert ei.value.status == B.CA_ERR_INVALID
+
+
+def test_wrapper_rejects_bad_io_tensors():
+    """The torch wrapper refuses q/o (and K/V) tensors whose shape, dtype,
+    layout or device differ from what the kernels read and write, before any
+    launch; a correct call afterwards still matches the oracle."""
+    print("[case] wrapper argument checks", flush=True)
+    H, d, c = 2, 64, 4
+    p = Pair(c, H, d, np.float16, 256)
+    rng = np.random.default_rng(5)
+    for sid in range(3):
+        toks = rng.integers(0, 9, 7).astype(np.int32)
+        k, v = prefix_keyed_kv(5, toks, 0, H, d, np.float16)
+        p.insert(sid, toks, k, v)
+    B_ = p.cache.num_seqs()
+    q = to_dev(rng.standard_normal((B_, H, d)).astype(np.float16))
+    bad_outs = [torch.empty((B_ - 1, H, d), dtype=torch.float16, device="cuda"),
+                torch.empty((B_, H, d), dtype=torch.float32, device="cuda"),
+                torch.empty((B_, d, H), dtype=torch.float16, device="cuda").transpose(1, 2),
+                torch.empty((B_, H, d), dtype=torch.float16)]
+    for bad in bad_outs:
+        with pytest.raises(ValueError):
+            p.cache.attention(q, out=bad)
+        with pytest.raises(ValueError):
+            p.cache.prefill(0, q[:1].contiguous(), out=bad)
+    with pytest.raises(ValueError):
+        p.cache.attention(q.cpu())
+    with pytest.raises(ValueError):
+        p.cache.attention(q[:, :, :32].contiguous())
+    k_bad = torch.empty((1, H, d), dtype=torch.float16)
+    with pytest.raises(ValueError):
+        p.cache.append([0], [3], k_bad, k_bad)
+    o = p.cache.attention(q)
+    torch.cuda.synchronize()
+    assert_close(o.cpu().numpy(), p.reference(p.cache.seq_order(), q.cpu().numpy(), 0.0), np.float16,
+                 "after refused calls")
