@@ -9,6 +9,11 @@ from . import binding as B
 
 _DT = {torch.float16: B.CA_FP16, torch.float32: B.CA_FP32}
 
+# The current stream's raw handle without building a torch Stream object
+# (~0.3 us instead of ~3 us per call; the same call torch's own kernel
+# launchers use), falling back to the public API.
+_raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+
 
 class Cache:
     """A prefix-tree chunked KV cache on one GPU (or table-only on the host).
@@ -48,11 +53,14 @@ class Cache:
         else:
             raise ValueError(f"unknown layout {layout!r}")
         self._ws = None
+        self._dev_index = None if table_only else self.k_pool.device.index
 
     # -- helpers -----------------------------------------------------------
-    @staticmethod
-    def stream():
-        return torch.cuda.current_stream().cuda_stream
+    def stream(self):
+        """Handle of the current stream of the pools' device."""
+        if _raw_stream is not None:
+            return _raw_stream(self._dev_index)
+        return torch.cuda.current_stream(self._dev_index).cuda_stream
 
     def _kv(self, k, v, n):
         if self.table_only:
