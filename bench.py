@@ -54,6 +54,8 @@ def _parse():
     ap.add_argument("--no-prefill", action="store_true", help="skip the prefill-with-prefix-reuse timing")
     ap.add_argument("--dynamic-only", action="store_true",
                     help="run only the 64-step decode workload and print its figures (for profiling it)")
+    ap.add_argument("--prefill-only", action="store_true",
+                    help="run only the prefill join and print its figures (for profiling it)")
     ap.add_argument("--seg", type=int, default=0, help="chunk-first segment size (0: library default)")
     ap.add_argument("--split", type=int, default=-1, help="sequence-first split (-1: library default)")
     ap.add_argument("--schedule", type=int, default=-1,
@@ -70,6 +72,11 @@ def main():
         sys.exit(2)
     if args.dynamic_only:
         print(json.dumps({"dynamic": dynamic_run()}), flush=True)
+        return
+    if args.prefill_only:
+        import torch
+        torch.cuda.set_device(0)
+        print(json.dumps({"prefill": prefill_run()}), flush=True)
         return
 
     import numpy as np
