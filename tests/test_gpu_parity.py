@@ -502,3 +502,39 @@ def test_wrapper_rejects_bad_io_tensors():
     torch.cuda.synchronize()
     assert_close(o.cpu().numpy(), p.reference(p.cache.seq_order(), q.cpu().numpy(), 0.0), np.float16,
                  "after refused calls")
+
+
+@pytest.mark.parametrize("sched", [2, 4])
+def test_wide_batch_1024_rows(sched):
+    """A wide batch: 1,024 live sequences on a three-level tree (a 48-token
+    prompt, 32 branches of 20 tokens, unique suffixes of 1 to 40 tokens), so
+    shared runs cover up to 1,024 rows (64 chunk-first row blocks per
+    segment) and 4,096 (row, head) counters and partial slots are in use; a
+    leave, a join and one decode step, then sampled rows against the oracle,
+    tables bit-exact."""
+    print(f"[case] 1024-row batch schedule={sched}", flush=True)
+    rng = np.random.default_rng(1024 + sched)
+    H, d, c = 4, 64, 16
+    p = Pair(c, H, d, np.float16, 8192)
+    p.cache.set_tuning(schedule=sched)
+    prompt = rng.integers(0, 1000, 48).astype(np.int32)
+    branches = [rng.integers(1000 + 100 * b, 1100 + 100 * b, 20).astype(np.int32) for b in range(32)]
+    for sid in range(1024):
+        suffix = rng.integers(5000, 30000, int(rng.integers(1, 41))).astype(np.int32)
+        toks = np.concatenate([prompt, branches[sid % 32], suffix])
+        k, v = prefix_keyed_kv(77, toks, 0, H, d, np.float16)
+        p.insert(sid, toks, k, v)
+    p.remove(5)
+    toks = np.concatenate([prompt, branches[7], [29999, 29998]]).astype(np.int32)
+    k, v = prefix_keyed_kv(77, toks, 0, H, d, np.float16)
+    p.insert(5000, toks, k, v)
+    live = [int(s) for s in p.cache.seq_order()]
+    step_tok = rng.integers(0, 30000, len(live)).astype(np.int32)
+    kk = rng.standard_normal((len(live), H, d)).astype(np.float16)
+    vv = rng.standard_normal((len(live), H, d)).astype(np.float16)
+    p.append(live, step_tok, kk, vv)
+    p.check_tables()
+    qh = {s: rng.standard_normal((H, d)).astype(np.float16) for s in live}
+    o, q, row_seq = p.attention(qh)
+    rows = sorted(set([0, 1, len(row_seq) - 1] + [int(x) for x in rng.choice(len(row_seq), 40, replace=False)]))
+    assert_close(o[rows], p.reference(row_seq, q, 0.0, rows=rows), np.float16, f"1024 rows sched={sched}")
