@@ -538,3 +538,27 @@ def test_wide_batch_1024_rows(sched):
     o, q, row_seq = p.attention(qh)
     rows = sorted(set([0, 1, len(row_seq) - 1] + [int(x) for x in rng.choice(len(row_seq), 40, replace=False)]))
     assert_close(o[rows], p.reference(row_seq, q, 0.0, rows=rows), np.float16, f"1024 rows sched={sched}")
+
+
+@pytest.mark.parametrize("sched", [2, 4])
+def test_long_context_32k(sched):
+    """Long contexts: four rows of 32,768 tokens each (a 16,384-token shared
+    prompt, 256 chunks, then 16,384 private tokens per row), d = 128, c = 64:
+    the shared run is cut into many segments (each a partial per row, or a
+    fold into the row's accumulator under the partial-free schedule) and
+    every sequence-first row walks 256 private chunks. All rows against the
+    oracle."""
+    print(f"[case] 32k-token contexts schedule={sched}", flush=True)
+    rng = np.random.default_rng(32768 + sched)
+    H, d, c = 2, 128, 64
+    p = Pair(c, H, d, np.float16, 1400)
+    p.cache.set_tuning(schedule=sched)
+    prompt = rng.integers(0, 1000, 16384).astype(np.int32)
+    for sid in range(4):
+        toks = np.concatenate([prompt, rng.integers(1000 + 2000 * sid, 3000 + 2000 * sid, 16384)]).astype(np.int32)
+        k, v = prefix_keyed_kv(3, toks, 0, H, d, np.float16)
+        p.insert(sid, toks, k, v)
+    p.check_tables()
+    qh = {s: rng.standard_normal((H, d)).astype(np.float16) for s in range(4)}
+    o, q, row_seq = p.attention(qh)
+    assert_close(o, p.reference(row_seq, q, 0.0), np.float16, f"32k contexts sched={sched}")

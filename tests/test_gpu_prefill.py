@@ -113,3 +113,25 @@ def test_prefill_long_paths(c, L):
         torch.cuda.synchronize()
         ref = prefill_attention(p.tree, 0, q, 1.0 / np.sqrt(d))
         assert_close(o.cpu().numpy(), ref, np.float16, f"prefill c={c} L={L} n_q={n_q}")
+
+
+def test_prefill_long_context():
+    """A long join: 2,048 new tokens after a 6,144-token cached prefix (an
+    8,192-token path of 128 chunks), sampled queries against the oracle,
+    including the first, the last and the 64-query tile boundaries."""
+    print("[case] prefill of 2048 new tokens over 8192 positions", flush=True)
+    rng = np.random.default_rng(8192)
+    H, d, c = 2, 128, 64
+    p = Pair(c, H, d, np.float16, 400)
+    prefix = rng.integers(0, 500, 6144).astype(np.int32)
+    k, v = prefix_keyed_kv(8, prefix, 0, H, d, np.float16)
+    p.insert(0, prefix, k, v)
+    toks = np.concatenate([prefix, rng.integers(500, 1000, 2048)]).astype(np.int32)
+    k, v = prefix_keyed_kv(8, toks, 0, H, d, np.float16)
+    assert p.insert(1, toks, k, v) == 6144
+    q = rng.standard_normal((2048, H, d)).astype(np.float16)
+    o = p.cache.prefill(1, to_dev(q)).cpu().numpy()
+    rows = sorted({0, 1, 63, 64, 127, 128, 1023, 1024, 2046, 2047} |
+                  {int(x) for x in rng.choice(2048, 20, replace=False)})
+    ref = prefill_attention(p.tree, 1, q, 1.0 / np.sqrt(d), queries=rows)
+    assert_close(o[rows], ref, np.float16, "prefill 2048 over 8192")
