@@ -294,30 +294,34 @@ def prefill_run(n=100):
     for s in wl.seqs + [pj.seq]:
         matched = cache.insert(s.seq_id, s.tokens(wl.segments), torch.cat([seg_dev[i][0] for i in s.segs]),
                                torch.cat([seg_dev[i][1] for i in s.segs]))
-    q = torch.from_numpy(pj.q).cuda()
-    o = torch.empty_like(q)
     sid = pj.seq.seq_id
-
-    def call():
-        cache.prefill(sid, q, out=o)
-
-    call()
-    torch.cuda.synchronize()
-    a = torch.cuda.Event(enable_timing=True)
-    b = torch.cuda.Event(enable_timing=True)
-    torch.cuda._sleep(40_000_000)   # hold the stream while the calls are enqueued
-    a.record()
-    for _ in range(n):
-        call()
-    b.record()
-    b.synchronize()
-    us = a.elapsed_time(b) * 1e3 / n
     L = len(pj.seq.tokens(wl.segments))
+
+    def timed(q):
+        o = torch.empty_like(q)
+        cache.prefill(sid, q, out=o)
+        torch.cuda.synchronize()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(40_000_000)   # hold the stream while the calls are enqueued
+        a.record()
+        for _ in range(n):
+            cache.prefill(sid, q, out=o)
+        b.record()
+        b.synchronize()
+        us = a.elapsed_time(b) * 1e3 / n
+        n_q = q.shape[0]
+        ctx = sum(L - n_q + i + 1 for i in range(n_q))  # attended positions over all queries
+        flops = 4 * wl.H * wl.d * ctx
+        return us, flops, flops / (us * 1e-6) / 1e12
+
+    q = torch.from_numpy(pj.q).cuda()
     n_q = pj.n_new
-    ctx = sum(L - n_q + i + 1 for i in range(n_q))      # attended positions over all queries
-    flops = 4 * wl.H * wl.d * ctx
+    us, flops, tflops = timed(q)
+    # a short join: only the last 64 tokens are new (two query tiles' worth of
+    # blocks per head at most, so the key range is split over blocks)
+    us64, flops64, tflops64 = timed(q[-64:].contiguous())
     kv_bytes = 2 * L * wl.H * wl.d * 2
-    tflops = flops / (us * 1e-6) / 1e12
     cache.close()
     del cache, seg_dev
     torch.cuda.empty_cache()
@@ -326,7 +330,9 @@ def prefill_run(n=100):
             "tok_per_s": n_q / (us * 1e-6), "flops": flops, "tflops": tflops,
             "roofline": {"bound": "mfma", "achieved": tflops, "peak": PEAK_MFMA_TFLOPS["f16"],
                          "unit": "TFLOP/s", "frac": tflops / PEAK_MFMA_TFLOPS["f16"]},
-            "kv_bytes": kv_bytes}
+            "kv_bytes": kv_bytes,
+            "short_join": {"n_q": 64, "us_per_call": us64, "flops": flops64, "tflops": tflops64,
+                           "kv_GBps": kv_bytes / (us64 * 1e-6) / 1e9}}
 
 
 def dynamic_run():

@@ -240,6 +240,14 @@ ca_status ca_prepare(ca_cache* cache, void* stream, int32_t* uploaded);
  * the K/V rows. The path (chunk slots and start positions, 8 bytes per
  * chunk) travels inside the kernel arguments for up to 255 chunks; a longer
  * one is copied to the device through library-owned pinned staging.
+ * Work is one block per (64 queries, head); when those blocks would leave
+ * compute units idle (a short join over a long path), each block's key
+ * range is cut into parts run by separate blocks, whose partial results
+ * (O, m, n) are folded by Eqn 2 in a library-owned device workspace
+ * (ceil(n_q / 64) * H * parts * (256 d + 512) bytes, grown on first need,
+ * which synchronizes the stream once). CA_PREFILL_SPLIT=k in the
+ * environment at ca_create forces k parts (1: never split); the results do
+ * not depend on it beyond fp32 summation order.
  * Errors: INVALID (table-only or fp32 cache, null or misaligned q/o,
  * n_q > L), NOT_FOUND, DEVICE. */
 ca_status ca_prefill_attention(ca_cache* cache, int64_t seq_id, const void* q, void* o,

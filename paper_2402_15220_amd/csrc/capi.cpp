@@ -166,6 +166,11 @@ struct ca_cache {
   size_t d_blob_cap = 0;
   int32_t* d_cnt = nullptr;  // [B][H] arrival counters of the partial-writing schedules
   size_t d_cnt_cap = 0;
+  int32_t prefill_split = 0;     // key-range parts of a prefill tile (0: automatic)
+  float* d_pf_ws = nullptr;      // prefill partials of split tiles
+  size_t d_pf_ws_cap = 0;
+  int32_t* d_pf_cnt = nullptr;   // prefill arrival counters, one per tile
+  size_t d_pf_cnt_cap = 0;
   PinnedStaging work_stage;     // kernel context uploads
   PinnedStaging prefill_stage;  // prefill paths
   PinnedStaging rowmap_stage;   // caller row orders
@@ -192,6 +197,8 @@ struct ca_cache {
     if (side.stream) (void)hipStreamDestroy(side.stream);
     if (d_path) (void)hipFree(d_path);
     if (d_rowmap) (void)hipFree(d_rowmap);
+    if (d_pf_ws) (void)hipFree(d_pf_ws);
+    if (d_pf_cnt) (void)hipFree(d_pf_cnt);
   }
 
   size_t esize() const { return cfg.dtype == CA_FP16 ? 2 : 4; }
@@ -330,23 +337,23 @@ struct ca_cache {
     return CA_OK;
   }
 
-  // Arrival counters for B*H (row, head) pairs. They are zeroed once when
-  // allocated; every launch leaves them at zero again.
-  ca_status ensure_counters(size_t n, hipStream_t stream) {
-    if (n <= d_cnt_cap) return CA_OK;
+  // At least n arrival counters in *p. They are zeroed once when allocated;
+  // every launch leaves them at zero again.
+  static ca_status ensure_counters(int32_t** p, size_t* cap_, size_t n, hipStream_t stream) {
+    if (n <= *cap_) return CA_OK;
     hipError_t e;
-    if (d_cnt) {
+    if (*p) {
       if ((e = hipStreamSynchronize(stream)) != hipSuccess) return hip_fail(e, "counter sync");
-      (void)hipFree(d_cnt);
-      d_cnt = nullptr;
-      d_cnt_cap = 0;
+      (void)hipFree(*p);
+      *p = nullptr;
+      *cap_ = 0;
     }
     const size_t cap = std::max<size_t>(n * 2, 1024);
-    if ((e = hipMalloc(reinterpret_cast<void**>(&d_cnt), cap * sizeof(int32_t))) != hipSuccess)
+    if ((e = hipMalloc(reinterpret_cast<void**>(p), cap * sizeof(int32_t))) != hipSuccess)
       return hip_fail(e, "counter alloc");
-    if ((e = ca::launch_fill_i32(d_cnt, static_cast<int64_t>(cap), 0, stream)) != hipSuccess)
+    if ((e = ca::launch_fill_i32(*p, static_cast<int64_t>(cap), 0, stream)) != hipSuccess)
       return hip_fail(e, "counter clear");
-    d_cnt_cap = cap;
+    *cap_ = cap;
     return CA_OK;
   }
 
@@ -419,6 +426,7 @@ ca_status ca_create(const ca_config* cfg, ca_cache** out) try {
   c->split_chunks = env_int("CA_SPLIT", 0);
   c->schedule = std::min(4, std::max(0, env_int("CA_SCHEDULE", 2)));
   c->check_patches = env_int("CA_CHECK_PATCH", 0) != 0;
+  c->prefill_split = std::min(64, std::max(0, env_int("CA_PREFILL_SPLIT", 0)));
   if (!c->table_only) {
     int dev = 0, cus = 0;
     if (hipGetDevice(&dev) == hipSuccess &&
@@ -589,7 +597,8 @@ static ca_status attention_impl(ca_cache* cache, const void* q, void* o, float s
     if (st != CA_OK) return st;
   }
   {
-    ca_status st = cache->ensure_counters(
+    ca_status st = ca_cache::ensure_counters(
+        &cache->d_cnt, &cache->d_cnt_cap,
         static_cast<size_t>(cache->tree.num_seqs()) * cache->cfg.num_heads, s);
     if (st != CA_OK) return st;
   }
@@ -729,6 +738,31 @@ ca_status ca_prefill_attention(ca_cache* cache, int64_t seq_id, const void* q, v
   a.n_q = static_cast<int>(n_q);
   const float sc = scale == 0.f ? 1.f / std::sqrt(static_cast<float>(a.D)) : scale;
   a.qscale = sc * 1.4426950408889634f;
+  // Key-range split: when the (64-query tile, head) blocks alone would leave
+  // compute units idle, cut each tile's units (64-row pieces of its chunks)
+  // into parts of at least six units, up to about one block per CU. The last
+  // part to finish folds all parts (about 1.3 us per part on a 64-token
+  // join over 1536 positions), so parts are kept long.
+  const int64_t tiles = (n_q + 63) / 64 * static_cast<int64_t>(a.H);
+  const int64_t units = static_cast<int64_t>(nc) * ((a.C + 63) / 64);
+  int64_t split = 1;
+  if (cache->prefill_split > 0)
+    split = cache->prefill_split;
+  else if (tiles < cache->num_cus)
+    split = std::min<int64_t>({(cache->num_cus + tiles - 1) / tiles, std::max<int64_t>(1, units / 6), 16});
+  a.n_split = static_cast<int>(split);
+  if (split > 1) {
+    const size_t ws = static_cast<size_t>(tiles * split) * ca::prefill_part_bytes(a.D);
+    if ((st = ensure_device(reinterpret_cast<char**>(&cache->d_pf_ws), &cache->d_pf_ws_cap, ws, s,
+                            "prefill partials")) != CA_OK)
+      return st;
+    if ((st = ca_cache::ensure_counters(&cache->d_pf_cnt, &cache->d_pf_cnt_cap,
+                                        static_cast<size_t>(tiles), s)) != CA_OK)
+      return st;
+    a.ws = cache->d_pf_ws;
+    a.ws_bytes = ws;
+    a.cnt = cache->d_pf_cnt;
+  }
   hipError_t e = ca::launch_prefill(a, s);
   if (e != hipSuccess) return hip_fail(e, "ca_prefill_attention launch");
   return CA_OK;

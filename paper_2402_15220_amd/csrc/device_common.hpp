@@ -116,5 +116,49 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 // vmcnt(0): every vector memory access of this wavefront has completed
 __device__ __forceinline__ void wait_stores() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
+// Device-scope (all XCDs) 4-byte stores and loads for data exchanged between
+// blocks of one launch, and the arrival protocol around them: a block's
+// threads store their part with st_dev, wait_stores(), meet at a barrier,
+// then one thread counts the block's arrival; the last of `need`
+// contributors gets true, resets the counter (so counters are zero between
+// launches) and reads the others' parts with ld_dev.
+__device__ __forceinline__ void st_dev(float* p, float x) {
+  __hip_atomic_store(p, x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_dev(const float* p) {
+  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ bool arrive_last(int32_t* c, int need) {
+  const int old = __hip_atomic_fetch_add(c, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (old != need - 1) return false;
+  __hip_atomic_store(c, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return true;
+}
+
+// Partials exchanged between blocks of one launch (possibly on different
+// XCDs, each with its own L2) use device-scope stores and loads (`sc1`):
+// they are coherent across XCDs per instruction, so no whole-cache writeback
+// or invalidate is needed. A writer waits for its stores to complete
+// (vmcnt(0)) before counting its arrival. Partial O vectors move as 16-byte
+// raw buffer accesses over the partial-O workspace (descriptor word 3 is the
+// gfx9 raw-buffer format; byte offsets are 32-bit, the host keeps that
+// region below 4 GiB).
+constexpr int kRsrcWord3 = 0x00020000;
+constexpr int kDevScope = 16;  // cache-policy bit sc1
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t part_rsrc(const float* ws_o, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(ws_o), 0, static_cast<int>(bytes),
+                                           kRsrcWord3);
+}
+__device__ __forceinline__ float4 ld_dev4(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<int>(off), 0, kDevScope);
+  return make_float4(__uint_as_float(v.x), __uint_as_float(v.y), __uint_as_float(v.z),
+                     __uint_as_float(v.w));
+}
+__device__ __forceinline__ void st_dev4(__amdgpu_buffer_rsrc_t r, uint32_t off, float a, float b,
+                                        float c, float d) {
+  const u32x4 v = {__float_as_uint(a), __float_as_uint(b), __float_as_uint(c), __float_as_uint(d)};
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, static_cast<int>(off), 0, kDevScope);
+}
+
 }  // namespace
 }  // namespace ca

@@ -79,7 +79,16 @@ struct PrefillArgs {
   int n_chunks;
   int n_q;
   float qscale;  // softmax scale * log2(e)
+  // Key-range split of each (64-query tile, head): n_split parts in separate
+  // blocks; for n_split > 1, ws holds tiles * n_split partials of
+  // prefill_part_bytes(D) each and cnt one zeroed counter per tile
+  // (tiles = ceil(n_q / 64) * H); the kernel leaves the counters at zero.
+  int n_split = 1;
+  float* ws = nullptr;
+  size_t ws_bytes = 0;  // bytes of ws the launch may touch (below 4 GiB)
+  int32_t* cnt = nullptr;
 };
+constexpr size_t prefill_part_bytes(int D) { return (64 * static_cast<size_t>(D) + 128) * 4; }
 hipError_t launch_prefill(const PrefillArgs& a, hipStream_t stream);
 
 // p[0 .. n) = value on `stream` (a kernel, not a memset node).

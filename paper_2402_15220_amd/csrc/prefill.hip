@@ -36,6 +36,11 @@ namespace {
 //                 accumulators of two token tiles as B).
 // At the end the groups' states (m, n, O) are folded (Eqn 2) through LDS
 // and group 0 writes o = O / n.
+// When the query tiles alone would leave most compute units idle (a short
+// join over a long path), each tile's units are cut into n_split contiguous
+// parts run by separate blocks: every part writes its (m, n, O) with
+// device-scope stores and counts its arrival, and the last part to arrive
+// folds all of them (Eqn 2) and writes o; nobody waits for anybody.
 struct KpfParams {
   const _Float16* q;            // [n_q][H][D]
   _Float16* o;                  // [n_q][H][D]
@@ -49,7 +54,19 @@ struct KpfParams {
   int H;
   int C;
   float qscale;                 // softmax scale * log2(e)
+  int n_split;                  // key-range parts per (query tile, head); 1: none
+  float* ws;                    // n_split > 1: one partial per part, [tile][part] of
+                                // kpf_part_floats<D>() floats: O [64][D], then m [64], n [64]
+  int32_t* cnt;                 // n_split > 1: arrival counter per tile, zero between launches
+  uint32_t ws_bytes;            // bytes of ws (below 4 GiB: 32-bit buffer offsets)
 };
+
+// floats of one partial: unnormalised O of 64 query rows, their maxima and sums
+template <int D>
+constexpr int kpf_part_floats() { return 64 * D + 2 * 64; }
+static_assert(prefill_part_bytes(128) == kpf_part_floats<128>() * 4 &&
+                  prefill_part_bytes(64) == kpf_part_floats<64>() * 4,
+              "partial size shared with the host");
 
 template <int D>
 constexpr int kpf_k_stride() { return D + 8; }
@@ -186,10 +203,12 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
   const int n_qt = (n_q + 63) / 64;
   const int per_xcd = static_cast<int>(gridDim.x) / 8;
   const int v = static_cast<int>(blockIdx.x % 8) * per_xcd + static_cast<int>(blockIdx.x / 8);
-  if (v >= n_qt * H) return;
-  const int h = v / n_qt;
+  const int S = P.n_split;
+  if (v >= n_qt * H * S) return;
+  const int tix = v / S, part = v % S;   // the parts of a tile are neighbours (same XCD)
+  const int h = tix / n_qt;
   const int L = chunk_end(P.n_chunks - 1);
-  const int q0 = (v % n_qt) * 64;                              // first query of the tile
+  const int q0 = (tix % n_qt) * 64;                            // first query of the tile
   const int pos_last = L - n_q + min(q0 + 63, n_q - 1);        // last position of the tile
   const int pos_first = L - n_q + q0;                          // first position of the tile
   const size_t slot_stride = static_cast<size_t>(P.ss);
@@ -241,6 +260,9 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
     }
   }
   const int n_units = n_ch * upc;
+  // this block's part of the tile's units
+  const int u_lo = static_cast<int>(static_cast<int64_t>(n_units) * part / S);
+  const int u_hi = static_cast<int>(static_cast<int64_t>(n_units) * (part + 1) / S);
   // unit u is rows r0 .. r0 + TOK - 1 of chunk j (no division when every
   // chunk is one unit; uniform)
   auto unit_pos = [&](int u, int& j, int& r0) {
@@ -258,7 +280,7 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
   u32x4 kr[GPT], vr[GPT];
   auto issue = [&](int u) {
     int j, r0;
-    unit_pos(min(u, n_units - 1), j, r0);
+    unit_pos(min(u, u_hi - 1), j, r0);
     kpf_load_rows<D, GT, TOK>(kbase, vbase, slot_stride, chunk_slot(j), r0,
                               chunk_end(j) - chunk_start(j), gtid, kr, vr);
   };
@@ -375,24 +397,25 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
       }
     }
   };
-  // Two LDS tiles per group: step i computes the group's unit i from tile
-  // i % 2 while unit i + 1 is written into the other tile and unit i + 2
-  // loads into the registers; one barrier per step (after it, tile i % 2 is
-  // complete and nobody still reads the other one).
-  const int steps = (n_units + NGRP - 1) / NGRP;  // the same in every group
+  // Two LDS tiles per group: step i computes the group's unit i of the part
+  // (unit u_lo + grp + i * NGRP) from tile i % 2 while unit i + 1 is written
+  // into the other tile and unit i + 2 loads into the registers; one barrier
+  // per step (after it, tile i % 2 is complete and nobody still reads the
+  // other one).
+  const int steps = (u_hi - u_lo + NGRP - 1) / NGRP;  // the same in every group
   if (steps > 0) {
-    issue(grp);
+    issue(u_lo + grp);
     stage(0);
-    issue(grp + NGRP);
+    issue(u_lo + grp + NGRP);
   }
   for (int i = 0; i < steps; ++i) {
     __syncthreads();
     if (i + 1 < steps) {
       stage((i + 1) & 1);
-      issue(grp + (i + 2) * NGRP);
+      issue(u_lo + grp + (i + 2) * NGRP);
     }
-    const int u = grp + i * NGRP;
-    if (u < n_units) compute(u, i & 1);
+    const int u = u_lo + grp + i * NGRP;
+    if (u < u_hi) compute(u, i & 1);
   }
   // row sums over the four lane groups
   float n_row[QT];
@@ -420,9 +443,9 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
       }
     }
     __syncthreads();
-    if (grp > 0) return;
 #pragma unroll
     for (int t = 0; t < QT; ++t) {
+      if (grp > 0) break;
       const int r = 16 * (QT * w + t) + l16;
 #pragma unroll
       for (int k = 1; k < NGRP; ++k) {
@@ -438,19 +461,110 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
       }
     }
   }
+  if (S == 1) {
+    if (grp > 0) return;
 #pragma unroll
-  for (int t = 0; t < QT; ++t) {
-    if (qi[t] < n_q) {
-      const float inv = 1.f / n_row[t];
-      _Float16* out = P.o + (static_cast<size_t>(qi[t]) * H + h) * D;
+    for (int t = 0; t < QT; ++t) {
+      if (qi[t] < n_q) {
+        const float inv = 1.f / n_row[t];
+        _Float16* out = P.o + (static_cast<size_t>(qi[t]) * H + h) * D;
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        half4 r4;
+        for (int dt = 0; dt < DT; ++dt) {
+          half4 r4;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) r4[i] = static_cast<_Float16>(acc[t][dt][i] * inv);
-        *reinterpret_cast<half4*>(out + 16 * dt + 4 * g) = r4;
+          for (int i = 0; i < 4; ++i) r4[i] = static_cast<_Float16>(acc[t][dt][i] * inv);
+          *reinterpret_cast<half4*>(out + 16 * dt + 4 * g) = r4;
+        }
       }
     }
+    return;
+  }
+  // A part of a split tile: group 0 publishes the block's (O, m, n) for the
+  // tile's 64 rows (device-scope stores), the block counts its arrival, and
+  // the last of the S parts folds all of them (Eqn 2: common maximum, each
+  // part's sum and O rescaled) and writes o = O / n.
+  constexpr int PF = kpf_part_floats<D>();
+  constexpr int NT = 64 * WPG * NGRP;  // threads of the block
+  const __amdgpu_buffer_rsrc_t rs = part_rsrc(P.ws, P.ws_bytes);
+  if (grp == 0) {
+    const uint32_t pw = static_cast<uint32_t>((static_cast<size_t>(tix) * S + part) * PF);
+#pragma unroll
+    for (int t = 0; t < QT; ++t) {
+      const int r = 16 * (QT * w + t) + l16;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+        st_dev4(rs, 4 * (pw + r * D + 16 * dt + 4 * g), acc[t][dt][0], acc[t][dt][1], acc[t][dt][2],
+                acc[t][dt][3]);
+      if (g == 0) {
+        st_dev(P.ws + pw + 64 * D + r, m_run[t]);
+        st_dev(P.ws + pw + 64 * D + 64 + r, n_row[t]);
+      }
+    }
+  }
+  wait_stores();
+  __syncthreads();  // every store of the block's part has completed
+  __shared__ int last_part;
+  if (tid == 0) last_part = arrive_last(P.cnt + tix, S);
+  __syncthreads();
+  if (!last_part) return;
+  // The last part folds, online over batches of KB parts (Eqn 2 per output
+  // item: running maximum, sum and O rescaled at each batch); each batch's
+  // loads (O, m and n of every item's row in every part) are in flight
+  // together.
+  const size_t pt = static_cast<size_t>(tix) * S * PF;
+  constexpr int IPT = 64 * (D / 4) / NT;  // 4-column items per thread
+  constexpr int KB = 4;
+  static_assert(IPT * NT == 64 * (D / 4), "fold items");
+  float4 o4[IPT];
+  float mx[IPT], nx[IPT];
+#pragma unroll
+  for (int j = 0; j < IPT; ++j) {
+    o4[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+    mx[j] = kNegBig;
+    nx[j] = 0.f;
+  }
+  for (int k0 = 0; k0 < S; k0 += KB) {
+    float mk[KB][IPT], nk[KB][IPT];
+    float4 vk[KB][IPT];
+#pragma unroll
+    for (int kk = 0; kk < KB; ++kk) {
+      if (k0 + kk >= S) break;
+      const size_t base = pt + static_cast<size_t>(k0 + kk) * PF;
+#pragma unroll
+      for (int j = 0; j < IPT; ++j) {
+        const int e = tid + NT * j, r = e / (D / 4), d0 = 4 * (e % (D / 4));
+        mk[kk][j] = ld_dev(P.ws + base + 64 * D + r);
+        nk[kk][j] = ld_dev(P.ws + base + 64 * D + 64 + r);
+        vk[kk][j] = ld_dev4(rs, static_cast<uint32_t>(4 * (base + r * D + d0)));
+      }
+    }
+#pragma unroll
+    for (int kk = 0; kk < KB; ++kk) {
+      if (k0 + kk >= S) break;
+#pragma unroll
+      for (int j = 0; j < IPT; ++j) {
+        const float M = fmaxf(mx[j], mk[kk][j]);
+        const float a = fast_exp2(mx[j] - M), b = fast_exp2(mk[kk][j] - M);
+        o4[j].x = o4[j].x * a + vk[kk][j].x * b;
+        o4[j].y = o4[j].y * a + vk[kk][j].y * b;
+        o4[j].z = o4[j].z * a + vk[kk][j].z * b;
+        o4[j].w = o4[j].w * a + vk[kk][j].w * b;
+        nx[j] = nx[j] * a + nk[kk][j] * b;
+        mx[j] = M;
+      }
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < IPT; ++j) {
+    const int e = tid + NT * j, r = e / (D / 4), d0 = 4 * (e % (D / 4));
+    if (q0 + r >= n_q) continue;
+    const float f = 1.f / nx[j];
+    half4 r4;
+    r4[0] = static_cast<_Float16>(o4[j].x * f);
+    r4[1] = static_cast<_Float16>(o4[j].y * f);
+    r4[2] = static_cast<_Float16>(o4[j].z * f);
+    r4[3] = static_cast<_Float16>(o4[j].w * f);
+    *reinterpret_cast<half4*>(P.o + (static_cast<size_t>(q0 + r) * H + h) * D + d0) = r4;
   }
 }
 
@@ -460,14 +574,17 @@ hipError_t launch_prefill(const PrefillArgs& a, hipStream_t stream) {
   if (a.n_q <= 0 || a.n_chunks <= 0) return hipSuccess;
   KpfParams P{static_cast<const _Float16*>(a.q), static_cast<_Float16*>(a.o),
               static_cast<const _Float16*>(a.kpool), static_cast<const _Float16*>(a.vpool), a.ss,
-              a.hs, a.n_chunks, a.n_q, a.H, a.C, a.qscale};
+              a.hs, a.n_chunks, a.n_q, a.H, a.C, a.qscale, a.n_split, a.ws, a.cnt,
+              static_cast<uint32_t>(a.ws_bytes)};
+  if (a.n_split < 1 || (a.n_split > 1 && (!a.ws || !a.cnt || a.ws_bytes > 0xFFFFFFF0ull)))
+    return hipErrorInvalidValue;
   // two groups of four wavefronts (16 queries each), 64-row units, two LDS
   // tiles per group
   constexpr int kGroups = 2, kWaves = 4, kTok = 64;
   // paths up to this long keep their chunk table in the lanes of a register
   constexpr int kLaneChunks = 64;
-  const int tiles = ((a.n_q + 63) / 64) * a.H;
-  const dim3 grid(8 * ((tiles + 7) / 8));  // a multiple of the XCD count
+  const int blocks = ((a.n_q + 63) / 64) * a.H * a.n_split;
+  const dim3 grid(8 * ((blocks + 7) / 8));  // a multiple of the XCD count
   const dim3 block(64 * kWaves * kGroups);
   if (a.host_path && a.n_chunks <= kLaneChunks) {
     KpfPath<kLaneChunks> path;
