@@ -137,8 +137,9 @@ def test_prefill_long_context():
     assert_close(o[rows], ref, np.float16, "prefill 2048 over 8192")
 
 
-@pytest.mark.parametrize("split", [1, 2, 3, 5, 16])
-def test_prefill_key_range_split(split, monkeypatch):
+@pytest.mark.parametrize("split,layout", [(1, "split"), (2, "split"), (3, "split"), (5, "split"),
+                                          (16, "split"), (3, "interleaved")])
+def test_prefill_key_range_split(split, layout, monkeypatch):
     """The key-range split of a tile over several blocks (partials folded by
     the last part to arrive), forced to 1, 2, 3, 5 and 16 parts through
     CA_PREFILL_SPLIT: paths of 24 chunks of 64 (kernel-argument table in
@@ -147,11 +148,11 @@ def test_prefill_key_range_split(split, monkeypatch):
     head sizes."""
     import os
     monkeypatch.setenv("CA_PREFILL_SPLIT", str(split))
-    print(f"[case] prefill split={split}", flush=True)
+    print(f"[case] prefill split={split} layout={layout}", flush=True)
     rng = np.random.default_rng(4000 + split)
     for c, L, n_qs, d, H in [(64, 1536, (1, 64, 100, 512), 128, 2), (16, 1120, (7, 129), 64, 3),
                              (1, 300, (3, 300), 64, 1), (64, 300, (5,), 128, 1)]:
-        p = Pair(c, H, d, np.float16, 2 * (L // c + 2))
+        p = Pair(c, H, d, np.float16, 2 * (L // c + 2), layout=layout)
         toks = rng.integers(0, 50, L).astype(np.int32)
         k, v = prefix_keyed_kv(split, toks, 0, H, d, np.float16)
         p.insert(0, toks, k, v)
@@ -160,6 +161,6 @@ def test_prefill_key_range_split(split, monkeypatch):
             o = p.cache.prefill(0, to_dev(q)).cpu().numpy()
             rows = sorted({0, n_q - 1, n_q // 2} | {int(x) for x in rng.integers(0, n_q, 6)})
             ref = prefill_attention(p.tree, 0, q, 1.0 / np.sqrt(d), queries=rows)
-            assert_close(o[rows], ref, np.float16, f"split={split} c={c} L={L} n_q={n_q} d={d}")
+            assert_close(o[rows], ref, np.float16, f"split={split} {layout} c={c} L={L} n_q={n_q} d={d}")
         p.cache.close()
     assert os.environ["CA_PREFILL_SPLIT"] == str(split)
