@@ -40,7 +40,7 @@ namespace {
 // join over a long path), each tile's units are cut into n_split contiguous
 // parts run by separate blocks: every part writes its (m, n, O) with
 // device-scope stores and counts its arrival, and the last part to arrive
-// folds all of them (Eqn 2) and writes o; nobody waits for anybody.
+// folds all of them (Eqn 2) and writes o; no block waits for another.
 struct KpfParams {
   const _Float16* q;            // [n_q][H][D]
   _Float16* o;                  // [n_q][H][D]
@@ -195,10 +195,11 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
   const int l16 = lane & 15, g = lane >> 4;
   // the group's two tiles: tile b holds K rows then V rows
   auto tile_k = [&](int b) { return reinterpret_cast<_Float16*>(lds + (2 * grp + b) * TB); };
-  // XCD-aware tile order: blocks go to the eight XCDs round-robin, so block
-  // b runs on XCD b % 8; the tiles (head-major) are split into eight
-  // contiguous ranges, one per XCD, and every query tile of a head reads
-  // that head's chunks through the same L2.
+  // XCD-aware order: blocks go to the eight XCDs round-robin, so block b
+  // runs on XCD b % 8; the (tile, part) pairs (tiles head-major, the parts
+  // of a tile adjacent) are split into eight contiguous ranges, one per XCD,
+  // and every query tile of a head reads that head's chunks through the
+  // same L2.
   const int H = P.H, n_q = P.n_q;
   const int n_qt = (n_q + 63) / 64;
   const int per_xcd = static_cast<int>(gridDim.x) / 8;
