@@ -740,10 +740,10 @@ ca_status ca_prefill_attention(ca_cache* cache, int64_t seq_id, const void* q, v
   a.qscale = sc * 1.4426950408889634f;
   // Key-range split: when the (64-query tile, head) blocks alone would leave
   // compute units idle, cut each tile's units (64-row pieces of its chunks)
-  // into parts of at least six units, up to about one block per CU: each
-  // part adds fixed costs (its block's start, its partial's stores, its
-  // share of the last part's fold; about 1.3 us per part on a 64-token join
-  // over 1536 positions), so parts are kept long.
+  // into parts of at least six units, up to about one block per CU (one
+  // block fits a CU, so more blocks run in rounds): a part's time is mostly
+  // its block's fixed latency (start, first loads, merge, partial stores),
+  // so parts are kept long.
   const int64_t tiles = (n_q + 63) / 64 * static_cast<int64_t>(a.H);
   const int64_t units = static_cast<int64_t>(nc) * ((a.C + 63) / 64);
   int64_t split = 1;
