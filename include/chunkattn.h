@@ -4,11 +4,12 @@
  * two-phase partition of ChunkAttention (arXiv 2402.15220).
  *
  * Paper passages the calls follow:
- *   - Section 3.1 (PAKV): the KV cache is a forest of chunks, each holding at
- *     most c tokens and the K and V slices of those tokens; a joining sequence
- *     inserts a path (with prefix lookup), a leaving sequence deletes its
- *     path, and decoding appends one token per sequence, growing a new chunk
- *     when the leaf chunk is full; chunks come from a pool with a free list.
+ *   - Section 3.1 (PAKV): the cache is a forest whose nodes are chunks of
+ *     up to c tokens with their K and V rows. Joining adds a root-to-leaf
+ *     path after looking up the longest cached prefix; leaving deletes the
+ *     sequence's path; a decode step adds one token to each sequence's last
+ *     chunk, or a fresh child chunk once that one has no room. Chunk storage
+ *     is recycled through a free list.
  *   - Section 3.2 (TPP): attention for the last token of every live sequence,
  *     Q in R^{b x d} per head (Algorithms 1 and 2, Eqn 1 and Eqn 2).
  *   - Section 3.3: the kernel context (chunk, first and last covered query

@@ -166,6 +166,10 @@ class OracleTree:
 
     # -- operations --------------------------------------------------------
     def match(self, tokens) -> int:
+        """Prefix lookup (Section 3.2, prefill paragraph): R2's descent
+        without any change to the tree. Returns how many leading tokens are
+        already stored, counting a partial match inside the chunk where the
+        descent stops."""
         tokens = np.asarray(tokens, np.int32)
         _, pos, _ = self._descend(self.root, tokens, 0)
         return pos

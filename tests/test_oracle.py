@@ -13,6 +13,7 @@ import torch
 
 from oracle import (OracleTree, PoolExhausted, dense_attention, dense_attention_rows,
                     path_kv, prefill_attention, structured_attention, tables)
+from prefix_util import max_lcp, probes
 from workloads import make_dynamic, make_static, prefix_keyed_kv, random_op_script
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
@@ -177,6 +178,117 @@ def test_random_scripts_keep_invariants(seed):
                 if tb.node_row_begin[i] <= r < tb.node_row_end[i]:
                     path_len += int(tb.node_len[i])
             assert path_len == t.length[sid]
+
+
+# -- prefix lookup (Section 3.2, prefill paragraph) ---------------------------
+
+def test_match_on_fig2_tree_hand_values():
+    """Figure 2's tree (c=4; shared 10..21, S0 +30..33, S1 +40..47, S2 +50..57):
+    lookups that end inside a shared chunk, at chunk boundaries, inside a
+    private chunk, at the end of a path, past it, and on the first token."""
+    t = _fig2_tree()
+    shared = list(range(10, 22))
+    cases = [
+        ([10, 11, 12, 99], 3),                          # inside C0
+        ([10, 11, 12, 13], 4),                          # end of C0
+        (list(range(10, 16)) + [99], 6),                # inside C1
+        (shared, 12),                                   # end of the shared run
+        (shared + [40, 41, 99], 14),                    # inside C4 (S1's first private chunk)
+        (shared + list(range(40, 44)), 16),             # end of C4
+        (shared + list(range(40, 48)), 20),             # exactly S1
+        (shared + list(range(40, 48)) + [1, 2, 3], 20),  # past S1's path
+        (shared + [50, 51, 52, 53, 54, 99], 17),        # inside C7
+        (shared + [30, 31, 32, 33, 34], 16),            # past S0
+        (shared + [31], 12),                            # no child starts with 31
+        ([11, 12], 0),                                  # not a root prefix
+        ([99], 0),
+        ([10], 1),
+    ]
+    for probe, want in cases:
+        assert t.match(probe) == want, (probe, want)
+
+
+def test_match_on_split_example_hand_values():
+    """c=4, A=[1..6] then B=[1,2,9]; then A leaves: lookups across the split
+    node X=[1,2] / X'=[3,4], and after the removal frees X' and Y."""
+    t = OracleTree(c=4, with_kv=False)
+    t.insert(0, [1, 2, 3, 4, 5, 6])
+    assert t.match([1, 2, 3, 7]) == 3          # inside the chunk before any split
+    assert t.match([1, 2, 3, 4, 5, 6, 7]) == 6
+    t.insert(1, [1, 2, 9])
+    assert t.match([1, 2]) == 2                # end of X
+    assert t.match([1, 2, 3]) == 3             # inside X'
+    assert t.match([1, 2, 3, 4, 7]) == 4       # end of X'
+    assert t.match([1, 2, 3, 4, 5, 9]) == 5    # inside Y
+    assert t.match([1, 2, 9, 9]) == 3          # past B's path
+    assert t.match([1, 9]) == 1
+    t.remove(0)
+    assert t.match([1, 2, 3]) == 2             # X' and Y were freed
+    assert t.match([1, 2, 9]) == 3
+
+
+def _match_script_check(t, live, rng, alphabet, n_probes=12):
+    for p in probes(rng, list(live.values()), n_probes, alphabet):
+        assert t.match(p) == max_lcp(live.values(), p), (p, t.match(p))
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_match_is_longest_common_prefix_with_live_sequences(seed):
+    """After every operation of a random script, the lookup of any probe equals
+    the longest common prefix of the probe with any live sequence, computed
+    by brute force from the sequences' own token lists (no tree)."""
+    c = [1, 2, 3, 4, 5, 7][seed % 6]
+    alphabet = 2 + seed % 3
+    t = OracleTree(c=c, with_kv=False)
+    live = {}
+    rng = np.random.default_rng(500 + seed)
+    for op in random_op_script(seed, n_ops=60, alphabet=alphabet, max_len=3 * c + 4):
+        if op[0] == "insert":
+            t.insert(op[1], op[2])
+            live[op[1]] = np.asarray(op[2], np.int32)
+        elif op[0] == "extend":
+            t.extend(op[1], op[2])
+            live[op[1]] = np.concatenate([live[op[1]], op[2]]).astype(np.int32)
+        elif op[0] == "append":
+            t.append_batch(op[1], op[2])
+            for sid, tok in zip(op[1], op[2]):
+                live[sid] = np.concatenate([live[sid], [tok]]).astype(np.int32)
+        else:
+            t.remove(op[1])
+            del live[op[1]]
+        _match_script_check(t, live, rng, alphabet)
+
+
+def _full_chunks_only_match(self, tokens):
+    """A plausible mistake: count only fully matched chunks, dropping a
+    partial match inside the chunk where the lookup stops."""
+    tokens = np.asarray(tokens, np.int32)
+    cur, pos = self.root, 0
+    while pos < tokens.shape[0]:
+        child = cur.children.get(int(tokens[pos]))
+        if child is None:
+            break
+        L = len(child)
+        if pos + L > tokens.shape[0] or not np.array_equal(child.tokens, tokens[pos:pos + L]):
+            break
+        cur, pos = child, pos + L
+    return pos
+
+
+@pytest.mark.parametrize("plant", ["full_chunks_only", "off_by_one"])
+def test_plant_match_mistakes_are_caught(monkeypatch, plant):
+    """The brute-force and hand-value pins catch a lookup that drops the
+    partial match inside the last chunk, and one that is off by one."""
+    import oracle.tree as T
+
+    good = T.OracleTree.match
+    bad = _full_chunks_only_match if plant == "full_chunks_only" else (
+        lambda self, tokens: max(0, good(self, tokens) - 1))
+    monkeypatch.setattr(T.OracleTree, "match", bad)
+    with pytest.raises(AssertionError):
+        test_match_on_fig2_tree_hand_values()
+    with pytest.raises(AssertionError):
+        test_match_is_longest_common_prefix_with_live_sequences(3)   # c = 4
 
 
 def test_memory_loss_bound():

@@ -12,6 +12,7 @@ import pytest
 
 from oracle import OracleTree, PoolExhausted, tables
 from paper_2402_15220_amd import binding as B
+from prefix_util import max_lcp, probes
 from workloads import make_dynamic, make_static, random_op_script
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -95,8 +96,10 @@ def test_random_scripts_bit_exact(seed):
     n_slots = slots if slots is not None else 1 << 20
     h = B.ca_create(c, 1, 64, B.CA_FP16, n_slots)
     t = OracleTree(c=c, num_slots=slots, with_kv=False)
-    live = set()
-    for op in random_op_script(seed, n_ops=80, alphabet=2 + seed % 3, max_len=3 * c + 4):
+    alphabet = 2 + seed % 3
+    live = {}                      # sid -> tokens, kept by the test itself
+    rng = np.random.default_rng(900 + seed)
+    for op in random_op_script(seed, n_ops=80, alphabet=alphabet, max_len=3 * c + 4):
         # keep the script valid when a NOMEM insert was refused
         if op[0] in ("extend", "remove") and op[1] not in live:
             continue
@@ -106,14 +109,24 @@ def test_random_scripts_bit_exact(seed):
                 continue
             op = ("append", ids, op[2][:len(ids)])
         err = _apply(h, t, op)
-        if op[0] == "insert" and err is None:
-            live.add(op[1])
-        if op[0] == "remove":
-            live.discard(op[1])
+        if err is None:
+            if op[0] == "insert":
+                live[op[1]] = np.asarray(op[2], np.int32)
+            elif op[0] == "extend":
+                live[op[1]] = np.concatenate([live[op[1]], op[2]]).astype(np.int32)
+            elif op[0] == "append":
+                for sid, tok in zip(op[1], op[2]):
+                    live[sid] = np.concatenate([live[sid], [tok]]).astype(np.int32)
+            else:
+                del live[op[1]]
         t.check_invariants()
         _same(B.ca_export_tables(h), tables(t))
         st = B.ca_stats(h)
         assert st["slots_used"] == t.slots_in_use()
+        # prefix lookup through the ABI: oracle and brute force agree with it
+        for p in probes(rng, list(live.values()), 6, alphabet):
+            got = B.ca_match(h, p)
+            assert got == t.match(p) == max_lcp(live.values(), p), (p, got)
     B.ca_destroy(h)
 
 
@@ -140,20 +153,59 @@ def test_dynamic_config_replay_bit_exact():
         toks = s.tokens(wl.segments)
         assert B.ca_insert(h, s.seq_id, toks) == t.insert(s.seq_id, toks)
     uploads_structural = 0
+    live = {s.seq_id: s.tokens(wl.segments) for s in wl.seqs}
+    rng = np.random.default_rng(55)
     for st in wl.steps():
         if st.churn:
             for sid in st.churn.removed:
                 B.ca_remove(h, sid)
                 t.remove(sid)
+                del live[sid]
             for s in st.churn.added:
                 toks = s.tokens(wl.segments)
+                # the join's prefix lookup finds exactly the shared prompt
+                assert B.ca_match(h, toks) == t.match(toks) == 2048
                 assert B.ca_insert(h, s.seq_id, toks) == t.insert(s.seq_id, toks) == 2048
+                live[s.seq_id] = toks
         B.ca_append_batch(h, st.live, st.tokens)
         t.append_batch(st.live, st.tokens)
+        for sid, tok in zip(st.live, st.tokens):
+            live[int(sid)] = np.concatenate([live[int(sid)], [tok]]).astype(np.int32)
         _same(B.ca_export_tables(h), tables(t))
         assert list(np.sort(B.ca_seq_order(h))) == list(st.live)
+        for p in probes(rng, list(live.values()), 4, 32000):
+            assert B.ca_match(h, p) == t.match(p) == max_lcp(live.values(), p)
         uploads_structural += 1
     t.check_invariants()
+    B.ca_destroy(h)
+
+
+def test_match_arguments_and_edge_cases():
+    """ca_match: refused arguments change nothing; an empty tree matches
+    nothing; a lookup may end inside a chunk (a split candidate) or run past
+    every stored path; a lookup never changes the tree."""
+    _lib_or_skip()
+    h = B.ca_create(4, 1, 64, B.CA_FP16, 4096)
+    assert B.ca_match(h, [1, 2, 3]) == 0
+    B.ca_insert(h, 0, [1, 2, 3, 4, 5, 6])
+    B.ca_insert(h, 1, [1, 2, 9])
+    before = B.ca_export_tables(h)
+    for bad in ([], [3, -1], [-5]):
+        with pytest.raises(B.ChunkAttnError) as ei:
+            B.ca_match(h, np.asarray(bad, np.int32))
+        assert ei.value.status == B.CA_ERR_INVALID
+    assert B.ca_match(h, [1, 2, 3]) == 3               # inside X' = [3, 4]
+    assert B.ca_match(h, [1, 2, 3, 4, 5, 6] + [7] * 1000) == 6
+    assert B.ca_match(h, [1, 2, 9, 9]) == 3
+    assert B.ca_match(h, [2]) == 0
+    long = np.arange(100000, dtype=np.int32)
+    B.ca_insert(h, 2, long[:5000])
+    assert B.ca_match(h, long) == 5000
+    assert B.ca_match(h, long[:4321]) == 4321
+    B.ca_remove(h, 2)
+    after = B.ca_export_tables(h)
+    for k in before:
+        assert np.array_equal(before[k], after[k]), k
     B.ca_destroy(h)
 
 
