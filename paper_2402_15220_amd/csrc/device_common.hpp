@@ -113,15 +113,46 @@ __device__ __forceinline__ float readlane_f(float x, int l) {
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-// vmcnt(0): every vector memory access of this wavefront has completed
-__device__ __forceinline__ void wait_stores() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+// Compiler-only barrier: emits no instruction, but no memory access is moved
+// across it (it pins the program order the exchange below relies on).
+__device__ __forceinline__ void compiler_fence() { __atomic_signal_fence(__ATOMIC_SEQ_CST); }
 
-// Device-scope (all XCDs) 4-byte stores and loads for data exchanged between
-// blocks of one launch, and the arrival protocol around them: a block's
-// threads store their part with st_dev, wait_stores(), meet at a barrier,
-// then one thread counts the block's arrival; the last of `need`
-// contributors gets true, resets the counter (so counters are zero between
-// launches) and reads the others' parts with ld_dev.
+// vmcnt(0): every vector memory access this wavefront issued before the call
+// has completed (for a device-scope store: it is visible to every XCD).
+__device__ __forceinline__ void wait_stores() {
+  compiler_fence();
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+  compiler_fence();
+}
+
+// Exchange of partial results between blocks of one launch (the blocks may
+// sit on different XCDs, whose L2 caches are not coherent with each other).
+// The HIP memory model would express it as a release fetch_add by each
+// writer and an acquire by the last one; at agent scope that costs a whole
+// L2 writeback and invalidate per block (measured 2.5x slower on the decode
+// call). The protocol below gets the same ordering per access instead:
+//  1. Writers store their part only with device-scope accesses (st_dev,
+//     st_dev4: the sc1 bit), which write through the XCD's L2, so a
+//     completed store is visible to loads from any XCD; nothing else the
+//     reader needs is stored by the writer.
+//  2. Every wavefront that stored waits for its stores to complete
+//     (wait_stores: s_waitcnt vmcnt(0)), and the block meets at a barrier
+//     (when more than one wavefront stored) before one thread counts the
+//     arrival with an atomic add at device scope (arrive_last). So the
+//     count is performed only after the whole part is visible.
+//  3. The thread whose add returns need - 1 is last: every other part was
+//     visible before its writer counted. The reader branches on that value
+//     before issuing any load of the parts (the hardware does not issue
+//     loads speculatively past a branch), and it reads them only with
+//     device-scope loads (ld_dev, ld_dev4: sc1), which do not return stale
+//     lines of its own L1 or L2.
+//  4. compiler_fence() in wait_stores and arrive_last keeps the compiler
+//     from sinking a part store below the wait or the count, or hoisting a
+//     part load above the count. Moving any part access across those
+//     points, or reading a part with an ordinary (non-sc1) load, breaks the
+//     protocol.
+// The last contributor also resets the counter to 0, so counters are zero
+// between launches (the next launch is ordered after it by the stream).
 __device__ __forceinline__ void st_dev(float* p, float x) {
   __hip_atomic_store(p, x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -129,20 +160,18 @@ __device__ __forceinline__ float ld_dev(const float* p) {
   return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ bool arrive_last(int32_t* c, int need) {
+  compiler_fence();
   const int old = __hip_atomic_fetch_add(c, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   if (old != need - 1) return false;
+  compiler_fence();
   __hip_atomic_store(c, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   return true;
 }
 
-// Partials exchanged between blocks of one launch (possibly on different
-// XCDs, each with its own L2) use device-scope stores and loads (`sc1`):
-// they are coherent across XCDs per instruction, so no whole-cache writeback
-// or invalidate is needed. A writer waits for its stores to complete
-// (vmcnt(0)) before counting its arrival. Partial O vectors move as 16-byte
-// raw buffer accesses over the partial-O workspace (descriptor word 3 is the
-// gfx9 raw-buffer format; byte offsets are 32-bit, the host keeps that
-// region below 4 GiB).
+// Partial O vectors move as 16-byte raw buffer accesses with the sc1 bit
+// (device scope; the exchange protocol above) over the partial-O workspace
+// (descriptor word 3 is the gfx9 raw-buffer format; byte offsets are
+// 32-bit, the host keeps that region below 4 GiB).
 constexpr int kRsrcWord3 = 0x00020000;
 constexpr int kDevScope = 16;  // cache-policy bit sc1
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t part_rsrc(const float* ws_o, uint32_t bytes) {

@@ -345,14 +345,19 @@ __device__ __forceinline__ void ksf_block(const KsfParams& P, int item, int h, c
       // If every other contributor of the row has already arrived (the usual
       // case: chunk-first items are dispatched first), fold their partials
       // straight into this item's state and finish the row: no partial, no
-      // arrival. The counter goes back to zero.
+      // arrival. The counter goes back to zero. This relies on the exchange
+      // protocol of device_common.hpp: a count of need - 1, read with a
+      // device-scope load, means every other part was visible before it was
+      // counted; the branch on it precedes every part load (the compiler
+      // fence keeps them there) and those loads are device-scope (fold_parts
+      // with DEV = true).
       const int k0 = P.part_ptr[it.row], k1 = P.part_ptr[it.row + 1];
       int32_t* c = P.cnt + static_cast<size_t>(it.row) * H + h;
       int ready = 0;
       if (lane == 0)
         ready = __hip_atomic_load(c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == k1 - k0 - 1;
       if (__shfl(ready, 0)) {
-        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        compiler_fence();
         fold_parts<EPL, 64 / LPT, true>(k0, k1, P.parts, P.ws_o, P.o_bytes, P.ws_ml, H, D, h,
                                         sub * EPL, lane, m, n, acc, it.out_part);
         if (lane == 0) __hip_atomic_store(c, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

@@ -3,6 +3,9 @@ library and in the oracle from one seeded workload, run the library's
 attention, and measure the error against the oracle's float64 result."""
 from __future__ import annotations
 
+import os
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 import torch
 
@@ -110,4 +113,25 @@ class Pair:
 
     def reference(self, row_seq, q, scale, rows=None):
         sc = scale if scale else 1.0 / np.sqrt(self.d)
-        return dense_attention_rows(self.tree, row_seq, q, sc, rows=rows)
+        return reference_rows(self.tree, row_seq, q, sc, rows=rows)
+
+
+def host_threads():
+    """Threads for the oracle: the CPUs this process may use, at most 16."""
+    return max(1, min(16, len(os.sched_getaffinity(0))))
+
+
+def reference_rows(tree, row_seq, q, scale, rows=None, threads=None):
+    """The oracle's dense_attention_rows for `rows`, the rows split over a
+    thread pool (NumPy releases the GIL in its copies and reductions); the
+    oracle code and its arithmetic are unchanged, each row is computed by one
+    call on one thread."""
+    rows = list(range(q.shape[0])) if rows is None else [int(r) for r in rows]
+    n = threads or host_threads()
+    if n <= 1 or len(rows) < 4:
+        return dense_attention_rows(tree, row_seq, q, scale, rows=rows)
+    per = -(-len(rows) // (2 * n))
+    groups = [rows[i:i + per] for i in range(0, len(rows), per)]
+    with ThreadPoolExecutor(n) as ex:
+        parts = list(ex.map(lambda g: dense_attention_rows(tree, row_seq, q, scale, rows=g), groups))
+    return np.concatenate(parts, axis=0)

@@ -21,4 +21,7 @@ from .synth import (  # noqa: F401
     make_prefill_join,
     PrefillJoin,
     decode_tokens,
+    make_sweep,
+    make_decode_run,
+    DecodeRun,
 )

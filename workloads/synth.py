@@ -22,6 +22,7 @@ Nothing here builds a tree or computes attention.
 from __future__ import annotations
 
 import dataclasses
+import os
 from typing import Iterator
 
 import numpy as np
@@ -333,6 +334,96 @@ def sweep_tokens(b: int, n_p: int, n_s: int, seed: int):
             t = np.zeros(0, np.int32)
         uniq.append(t)
     return shared, uniq
+
+
+def make_sweep(b: int, n_p: int, n_s: int, seed: int, H: int = 32, d: int = 128,
+               c: int = 64) -> StaticWorkload:
+    """One cell of the microkernel grid (Table 3): b prompts of n_p tokens
+    whose first n_s tokens are one shared prefix, fp16. Token ids from
+    ``sweep_tokens(b, n_p, n_s, seed)``; then, from PCG64(seed + 1), K and V
+    once per segment (the shared prefix, then each unique part) and q.
+    Segment i's K then V come from its own generator PCG64([seed, 1, i]), so
+    segments are drawn on several threads (NumPy releases the GIL while it
+    fills) with results independent of the thread count; q comes from
+    PCG64([seed, 2]). With n_s = n_p every sequence is the same prompt; with
+    n_s = 0 nothing is shared."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    dt = np.dtype(np.float16)
+    shared, uniq = sweep_tokens(b, n_p, n_s, seed)
+    seg_tokens = ([shared] if n_s > 0 else []) + [u for u in uniq if len(u) > 0]
+
+    def draw(i):
+        rng = np.random.Generator(np.random.PCG64([seed, 1, i]))
+        t = seg_tokens[i]
+        k = _draw_values(rng, (len(t), H, d), dt)
+        v = _draw_values(rng, (len(t), H, d), dt)
+        return Segment(t, k, v)
+
+    with ThreadPoolExecutor(max(1, min(16, len(os.sched_getaffinity(0))))) as ex:
+        segments = list(ex.map(draw, range(len(seg_tokens))))
+    rng = np.random.Generator(np.random.PCG64([seed, 2]))
+    base = 1 if n_s > 0 else 0
+    seqs = []
+    for i in range(b):
+        segs = ([0] if n_s > 0 else []) + ([base + i] if n_p > n_s else [])
+        seqs.append(Sequence(i, segs))
+    q = _draw_values(rng, (b, H, d), dt)
+    return StaticWorkload(0, f"sweep_b{b}_np{n_p}_ns{n_s}_h{H}_d{d}_c{c}_fp16", H, d, c, dt,
+                          1.0 / np.sqrt(d), segments, seqs, q, 0)
+
+
+@dataclasses.dataclass
+class DecodeRun:
+    """A batch decode run (Figure 3 / Figure 4): b sequences start as the
+    same n_s-token prompt and each step appends one token per sequence."""
+
+    name: str
+    H: int
+    d: int
+    c: int
+    dtype: np.dtype
+    scale: float
+    prompt: Segment
+    b: int
+    n_c: int
+    seed: int
+
+    def steps(self) -> Iterator[DecodeStep]:
+        """Step i: every sequence (ids 0..b-1) appends token [i, id] of
+        ``decode_tokens``, whose first step is redrawn where two sequences
+        would start with the same token (so each grows its own chunk); K, V
+        and q of the step from PCG64(seed + 1), in that order."""
+        toks = decode_tokens(self.b, self.n_c, self.seed)
+        if self.n_c > 0:
+            fix = np.random.Generator(np.random.PCG64(self.seed + 2))
+            seen = set()
+            for j in range(self.b):
+                while int(toks[0, j]) in seen:
+                    toks[0, j] = np.int32(fix.integers(0, VOCAB))
+                seen.add(int(toks[0, j]))
+        rng = np.random.Generator(np.random.PCG64(self.seed + 1))
+        ids = np.arange(self.b, dtype=np.int64)
+        for i in range(self.n_c):
+            k = _draw_values(rng, (self.b, self.H, self.d), self.dtype)
+            v = _draw_values(rng, (self.b, self.H, self.d), self.dtype)
+            q = _draw_values(rng, (self.b, self.H, self.d), self.dtype)
+            yield DecodeStep(i, None, ids, toks[i].copy(), k, v, q)
+
+
+def make_decode_run(b: int, n_s: int, n_c: int, seed: int, H: int = 32, d: int = 128,
+                    c: int = 64) -> DecodeRun:
+    """The batch-sweep workload (Figure 4: n_s shared prompt tokens, n_c
+    decode steps): prompt tokens from PCG64(seed), its K and V from
+    PCG64(seed + 3); the steps draw their own values."""
+    dt = np.dtype(np.float16)
+    rng = np.random.Generator(np.random.PCG64(seed))
+    prompt = rng.integers(0, VOCAB, size=n_s).astype(np.int32)
+    vr = np.random.Generator(np.random.PCG64(seed + 3))
+    k = _draw_values(vr, (n_s, H, d), dt)
+    v = _draw_values(vr, (n_s, H, d), dt)
+    return DecodeRun(f"decode_b{b}_ns{n_s}_nc{n_c}_h{H}_d{d}_c{c}_fp16", H, d, c, dt,
+                     1.0 / np.sqrt(d), Segment(prompt, k, v), b, n_c, seed)
 
 
 def decode_tokens(b: int, n_c: int, seed: int) -> np.ndarray:
