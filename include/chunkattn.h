@@ -215,6 +215,31 @@ ca_status ca_attention(ca_cache* cache, const void* q, void* o, float scale, voi
 ca_status ca_attention_ordered(ca_cache* cache, const void* q, void* o, const int64_t* seq_ids,
                                int64_t n, float scale, void* ws, size_t ws_bytes, void* stream);
 
+/* ca_attention for callers that cannot allocate memory: code being captured
+ * into a HIP graph, tight serving loops, harnesses that forbid hipMalloc.
+ * Same kernels, arguments (q, o in tree row order, scale) and result as
+ * ca_attention, but the partial results and arrival counters live in a
+ * device scratch array that is part of the library's code object: 16 MiB
+ * per GPU the library is loaded on, held until the process ends. The call
+ * itself allocates nothing (no hipMalloc, hipHostMalloc, hipFree, stream or
+ * event creation): it clears the counters with a kernel on `stream`, then
+ * launches the attention kernels.
+ *   Preconditions: the kernel context must already be on the device, i.e.
+ *   ca_prepare (or any attention call) after the last tree change that
+ *   altered the chunk structure and after the last ca_set_tuning; appends
+ *   that only fill existing chunks need nothing. Under schedule 3 one
+ *   ca_attention call must have created the second stream.
+ *   Limits: at most 65,536 (row, head) pairs (B * H) and 16,515,072 bytes
+ *   of partials (ca_workspace_size); larger calls return CA_ERR_WORKSPACE
+ *   and must use ca_attention with a caller workspace.
+ *   Sharing: every call on one GPU uses that GPU's one scratch array, so
+ *   calls that may overlap on one GPU (different streams, threads or
+ *   caches) race and give wrong results; serialise them.
+ * Errors: INVALID (table-only cache, null or misaligned q/o, bad scale,
+ * context not current, schedule 3 without its stream), WORKSPACE, DEVICE.
+ * B == 0 is a no-op. */
+ca_status ca_attention_noalloc(ca_cache* cache, const void* q, void* o, float scale, void* stream);
+
 /* Bring the kernel context up to date now (Section 3.3, further
  * optimizations: context generation hidden behind earlier GPU work). Builds
  * the tables and work lists for the current tree on the host and, if they

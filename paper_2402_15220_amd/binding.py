@@ -31,7 +31,7 @@ CA_FP32 = 1
 
 EXPORTED = ["ca_create", "ca_destroy", "ca_match", "ca_insert", "ca_extend", "ca_append_batch",
             "ca_remove", "ca_num_seqs", "ca_seq_order", "ca_workspace_size", "ca_attention",
-            "ca_attention_ordered", "ca_prefill_attention", "ca_prepare", "ca_export_tables", "ca_stats", "ca_set_tuning", "ca_last_error"]
+            "ca_attention_ordered", "ca_attention_noalloc", "ca_prefill_attention", "ca_prepare", "ca_export_tables", "ca_stats", "ca_set_tuning", "ca_last_error"]
 
 
 class ChunkAttnError(RuntimeError):
@@ -89,6 +89,7 @@ def load():
         "ca_prefill_attention": [vp, i64, vp, vp, i64, ctypes.c_float, vp],
         "ca_prepare": [vp, vp, ctypes.POINTER(i32)],
         "ca_attention_ordered": [vp, vp, vp, _P64, i64, ctypes.c_float, vp, ctypes.c_size_t, vp],
+        "ca_attention_noalloc": [vp, vp, vp, ctypes.c_float, vp],
         "ca_export_tables": [vp, ctypes.POINTER(CaTables)],
         "ca_stats": [vp, _P64, _P64, _P64, ctypes.POINTER(i32), ctypes.POINTER(i32), _P64],
         "ca_set_tuning": [vp, i32, i32, i32, i32],
@@ -196,6 +197,10 @@ def ca_attention_ordered(h, q, o, seq_ids, scale, ws, ws_bytes, stream=None):
     ids = np.ascontiguousarray(seq_ids, dtype=np.int64)
     _check(load().ca_attention_ordered(h, q, o, ids.ctypes.data_as(_P64), ids.shape[0],
                                        ctypes.c_float(scale), ws, ws_bytes, stream))
+
+
+def ca_attention_noalloc(h, q, o, scale, stream=None):
+    _check(load().ca_attention_noalloc(h, q, o, ctypes.c_float(scale), stream))
 
 
 def ca_prepare(h, stream=None) -> bool:

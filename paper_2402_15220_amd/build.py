@@ -28,7 +28,8 @@ COMMON = [
     "-Wall", "-Wno-unused-result", f"-I{INCLUDE}", f"-I{CSRC}",
 ]
 
-SOURCES = ["tree.cpp", "tables.cpp", "capi.cpp", "kernels.hip", "prefill.hip", "fill.hip"]
+SOURCES = ["tree.cpp", "tables.cpp", "capi.cpp", "kernels.hip", "prefill.hip", "fill.hip",
+           "scratch.hip"]
 
 
 def _compile(src: str, objdir: str) -> str:

@@ -152,6 +152,19 @@ class Cache:
                                    ws.data_ptr(), ws.numel(), self.stream())
         return out
 
+    def attention_noalloc(self, q, out, scale: float = 0.0):
+        """ca_attention_noalloc: q and out [B, H, d] in seq_order(), both
+        already allocated; the library allocates nothing for the call (its
+        partials live in a static device scratch). Needs the kernel context
+        on the device: call prepare() after structural tree changes."""
+        if self.table_only:
+            raise ValueError("table-only cache has no attention")
+        Bn = self.num_seqs()
+        self._check_rows(q, Bn, "q")
+        self._check_rows(out, Bn, "out")
+        B.ca_attention_noalloc(self.h, q.data_ptr(), out.data_ptr(), scale, self.stream())
+        return out
+
     def prefill(self, seq_id, q, out=None, scale: float = 0.0):
         """Causal attention of sequence ``seq_id``'s last q.shape[0] tokens over
         its whole K/V (prefill after a prefix-matched insert). q: [n_q, H, d]."""

@@ -183,6 +183,8 @@ struct ca_cache {
   ca::DevWork dw;
   bool dw_valid = false;
   int64_t uploads = 0;
+  char* scratch = nullptr;  // this device's copy of the static scratch (ca_attention_noalloc)
+  std::string scratch_error;  // why it is null
 
   // host export buffers
   ca::Tables exported;
@@ -436,6 +438,16 @@ ca_status ca_create(const ca_config* cfg, ca_cache** out) try {
     hipError_t e = hipMalloc(reinterpret_cast<void**>(&c->d_slot_len),
                              static_cast<size_t>(cfg->num_slots) * sizeof(int32_t));
     if (e == hipSuccess) e = hipMemset(c->d_slot_len, 0, static_cast<size_t>(cfg->num_slots) * 4);
+    if (e == hipSuccess) {
+      // this device's scratch address (once per device, this device current);
+      // only ca_attention_noalloc needs it, so a failure is reported there
+      const hipError_t se = ca::scratch_address(&c->scratch);
+      if (se != hipSuccess) {
+        c->scratch = nullptr;
+        c->scratch_error = hipGetErrorString(se);
+        (void)hipGetLastError();  // not left for a later launch check to find
+      }
+    }
     if (e != hipSuccess) {
       delete c;
       return hip_fail(e, "ca_create");
@@ -564,44 +576,23 @@ ca_status ca_workspace_size(const ca_cache* cache, size_t* bytes) try {
   return on_exception("ca_workspace_size");
 }
 
-static ca_status attention_impl(ca_cache* cache, const void* q, void* o, float scale, void* ws,
-                                size_t ws_bytes, void* stream, const int64_t* seq_ids,
-                                int64_t n) {
-  if (!cache) return fail(CA_ERR_INVALID, "ca_attention: null cache");
-  if (cache->table_only) return fail(CA_ERR_INVALID, "ca_attention: table-only cache");
-  if (seq_ids && n != cache->tree.num_seqs())
-    return fail(CA_ERR_INVALID, "ca_attention_ordered: n differs from the number of live sequences");
-  if (cache->tree.num_seqs() == 0) return CA_OK;
+// Arguments common to the attention entry points; nothing is changed when
+// they are refused.
+static ca_status check_attention_io(const ca_cache* cache, const void* q, void* o, float scale) {
   if (!q || !o) return fail(CA_ERR_INVALID, "ca_attention: null q/o");
   if ((reinterpret_cast<uintptr_t>(q) | reinterpret_cast<uintptr_t>(o)) & 15)
     return fail(CA_ERR_INVALID, "ca_attention: q/o must be 16-byte aligned");
   if (!(scale >= 0.f) || std::isinf(scale)) return fail(CA_ERR_INVALID, "ca_attention: bad scale");
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  cache->ensure_work();
-  const size_t need = cache->ws_bytes();
-  if (cache->work.n_parts > 0 && (!ws || ws_bytes < need || (reinterpret_cast<uintptr_t>(ws) & 255)))
-    return fail(CA_ERR_WORKSPACE, "ca_attention: workspace missing, misaligned or smaller than " +
-                                      std::to_string(need) + " bytes");
-  if (!cache->dw_valid) {
-    ca_status st = cache->upload(s);
-    if (st != CA_OK) return st;
-  }
-  const int32_t* row_map = nullptr;
-  if (seq_ids) {
-    ca_status st = cache->upload_row_map(seq_ids, n, s);
-    if (st != CA_OK) return st;
-    row_map = cache->d_rowmap;
-  }
-  if (cache->schedule == 3) {
-    ca_status st = cache->ensure_side();
-    if (st != CA_OK) return st;
-  }
-  {
-    ca_status st = ca_cache::ensure_counters(
-        &cache->d_cnt, &cache->d_cnt_cap,
-        static_cast<size_t>(cache->tree.num_seqs()) * cache->cfg.num_heads, s);
-    if (st != CA_OK) return st;
-  }
+  (void)cache;
+  return CA_OK;
+}
+
+// Enqueue the attention kernels for the uploaded kernel context. Partials
+// go to ws (partial O, then 256-byte aligned (m, n) pairs), arrival counters
+// to cnt (B * H of them, zero on entry; the kernels leave them zero).
+static ca_status launch_attention_call(ca_cache* cache, const void* q, void* o, float scale,
+                                       char* ws, int32_t* cnt, const int32_t* row_map,
+                                       hipStream_t s) {
   const float sc = scale == 0.f ? 1.f / std::sqrt(static_cast<float>(cache->cfg.head_dim)) : scale;
   ca::AttnArgs a{};
   a.dtype = cache->cfg.dtype == CA_FP16 ? 0 : 1;
@@ -620,17 +611,44 @@ static ca_status attention_impl(ca_cache* cache, const void* q, void* o, float s
   if (o_bytes > 0xFFFFFFFFull)
     return fail(CA_ERR_INVALID, "ca_attention: partial-O workspace above 4 GiB (" +
                                     std::to_string(o_bytes) + " bytes); use longer segments");
-  a.ws_o = static_cast<float*>(ws);
+  a.ws_o = reinterpret_cast<float*>(ws);
   a.ws_o_bytes = static_cast<uint32_t>(o_bytes);
-  a.ws_ml = np ? reinterpret_cast<float*>(static_cast<char*>(ws) +
-                                          align_up(np * a.H * a.D * 4, 256))
-               : nullptr;
+  a.ws_ml = np ? reinterpret_cast<float*>(ws + align_up(o_bytes, 256)) : nullptr;
   a.qscale = sc * 1.4426950408889634f;
-  a.cnt = cache->d_cnt;
+  a.cnt = cnt;
   a.row_map = row_map;
   hipError_t e = ca::launch_attention(a, cache->dw, s, cache->phase_mask, cache->side);
   if (e != hipSuccess) return hip_fail(e, "ca_attention launch");
   return CA_OK;
+}
+
+static ca_status attention_impl(ca_cache* cache, const void* q, void* o, float scale, void* ws,
+                                size_t ws_bytes, void* stream, const int64_t* seq_ids,
+                                int64_t n) {
+  if (!cache) return fail(CA_ERR_INVALID, "ca_attention: null cache");
+  if (cache->table_only) return fail(CA_ERR_INVALID, "ca_attention: table-only cache");
+  if (seq_ids && n != cache->tree.num_seqs())
+    return fail(CA_ERR_INVALID, "ca_attention_ordered: n differs from the number of live sequences");
+  if (cache->tree.num_seqs() == 0) return CA_OK;
+  ca_status st = check_attention_io(cache, q, o, scale);
+  if (st != CA_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  cache->ensure_work();
+  const size_t need = cache->ws_bytes();
+  if (cache->work.n_parts > 0 && (!ws || ws_bytes < need || (reinterpret_cast<uintptr_t>(ws) & 255)))
+    return fail(CA_ERR_WORKSPACE, "ca_attention: workspace missing, misaligned or smaller than " +
+                                      std::to_string(need) + " bytes");
+  if (!cache->dw_valid && (st = cache->upload(s)) != CA_OK) return st;
+  const int32_t* row_map = nullptr;
+  if (seq_ids) {
+    if ((st = cache->upload_row_map(seq_ids, n, s)) != CA_OK) return st;
+    row_map = cache->d_rowmap;
+  }
+  if (cache->schedule == 3 && (st = cache->ensure_side()) != CA_OK) return st;
+  st = ca_cache::ensure_counters(&cache->d_cnt, &cache->d_cnt_cap,
+                                 static_cast<size_t>(cache->tree.num_seqs()) * cache->cfg.num_heads, s);
+  if (st != CA_OK) return st;
+  return launch_attention_call(cache, q, o, scale, static_cast<char*>(ws), cache->d_cnt, row_map, s);
 }
 
 ca_status ca_attention(ca_cache* cache, const void* q, void* o, float scale, void* ws,
@@ -647,6 +665,48 @@ ca_status ca_attention_ordered(ca_cache* cache, const void* q, void* o, const in
   return attention_impl(cache, q, o, scale, ws, ws_bytes, stream, seq_ids ? seq_ids : &kNone, n);
 } catch (...) {
   return on_exception("ca_attention_ordered");
+}
+
+ca_status ca_attention_noalloc(ca_cache* cache, const void* q, void* o, float scale,
+                               void* stream) try {
+  if (!cache) return fail(CA_ERR_INVALID, "ca_attention_noalloc: null cache");
+  if (cache->table_only) return fail(CA_ERR_INVALID, "ca_attention_noalloc: table-only cache");
+  if (cache->tree.num_seqs() == 0) return CA_OK;
+  ca_status st = check_attention_io(cache, q, o, scale);
+  if (st != CA_OK) return st;
+  // Everything the call needs must exist already: the kernel context on the
+  // device (ca_prepare or an earlier attention call after the last tree or
+  // tuning change) and, for the two-stream schedule, its stream.
+  if (!cache->work_valid || cache->tree.dirty() || !cache->dw_valid)
+    return fail(CA_ERR_INVALID,
+                "ca_attention_noalloc: kernel context not current (call ca_prepare after the "
+                "last tree or tuning change)");
+  if (cache->schedule == 3 && !cache->side.stream)
+    return fail(CA_ERR_INVALID, "ca_attention_noalloc: the two-stream schedule's stream does not "
+                                "exist yet (one ca_attention call creates it)");
+  if (!cache->scratch)
+    return fail(CA_ERR_DEVICE, "ca_attention_noalloc: no device scratch: " + cache->scratch_error);
+  const size_t counters = static_cast<size_t>(cache->tree.num_seqs()) * cache->cfg.num_heads;
+  const size_t parts = cache->ws_bytes();
+  if (counters * sizeof(int32_t) > ca::kScratchCounterBytes ||
+      parts > ca::kScratchBytes - ca::kScratchCounterBytes)
+    return fail(CA_ERR_WORKSPACE,
+                "ca_attention_noalloc: the call needs " + std::to_string(counters) +
+                    " (row, head) counters and " + std::to_string(parts) +
+                    " bytes of partials; the device scratch holds " +
+                    std::to_string(ca::kScratchCounterBytes / sizeof(int32_t)) + " and " +
+                    std::to_string(ca::kScratchBytes - ca::kScratchCounterBytes) +
+                    " (use ca_attention with a caller workspace)");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int32_t* cnt = reinterpret_cast<int32_t*>(cache->scratch);
+  // the scratch keeps whatever the last call on this GPU left: the counters
+  // are cleared by a kernel on the caller's stream before every call
+  hipError_t e = ca::launch_fill_i32(cnt, static_cast<int64_t>(counters), 0, s);
+  if (e != hipSuccess) return hip_fail(e, "ca_attention_noalloc counter clear");
+  return launch_attention_call(cache, q, o, scale, cache->scratch + ca::kScratchCounterBytes, cnt,
+                               nullptr, s);
+} catch (...) {
+  return on_exception("ca_attention_noalloc");
 }
 
 ca_status ca_prepare(ca_cache* cache, void* stream, int32_t* uploaded) try {

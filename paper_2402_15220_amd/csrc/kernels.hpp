@@ -91,6 +91,14 @@ struct PrefillArgs {
 constexpr size_t prefill_part_bytes(int D) { return (64 * static_cast<size_t>(D) + 128) * 4; }
 hipError_t launch_prefill(const PrefillArgs& a, hipStream_t stream);
 
+// Device scratch of ca_attention_noalloc (scratch.hip): kScratchBytes per
+// GPU; the first kScratchCounterBytes hold arrival counters, the rest the
+// partial results. scratch_address() returns the current device's copy
+// (hipGetSymbolAddress, taken once per device).
+constexpr size_t kScratchBytes = size_t(16) << 20;
+constexpr size_t kScratchCounterBytes = size_t(256) << 10;
+hipError_t scratch_address(char** out);
+
 // p[0 .. n) = value on `stream` (a kernel, not a memset node).
 hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t value, hipStream_t stream);
 
