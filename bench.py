@@ -48,7 +48,10 @@ def _parse():
                          "unique tokens each (default), 3 = the same with a 4096-token prompt, "
                          "4 = two-level tree of 64 rows")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle sample time")
+    ap.add_argument("--cpu-seconds", type=float, default=8.0,
+                    help="target time of the oracle's all-cores sample of whole calls")
+    ap.add_argument("--no-other-configs", action="store_true",
+                    help="skip the warm and cold figures of the 4096-token-prompt and two-level trees")
     ap.add_argument("--no-cold", action="store_true", help="skip the cache-evicted timing")
     ap.add_argument("--no-dynamic", action="store_true", help="skip the 64-step decode workload")
     ap.add_argument("--no-prefill", action="store_true", help="skip the prefill-with-prefix-reuse timing")
@@ -82,27 +85,12 @@ def main():
     import numpy as np
     import torch
 
-    from paper_2402_15220_amd.cache import Cache
-    from paper_2402_15220_amd.roofline import PEAK_HBM_GBPS, PEAK_MFMA_TFLOPS, call_model
-    from workloads import make_static
+    from paper_2402_15220_amd.roofline import PEAK_HBM_GBPS, PEAK_MFMA_TFLOPS
 
     torch.cuda.set_device(0)
-    wl = make_static(args.config)
-    nodes = sum(-(-len(s) // wl.c) for s in wl.segments)
-    cache = Cache(wl.c, wl.H, wl.d, nodes + 16, dtype=torch.float16)
-    seg_dev = [(torch.from_numpy(s.k).cuda(), torch.from_numpy(s.v).cuda()) for s in wl.segments]
-    for s in wl.seqs:
-        cache.insert(s.seq_id, s.tokens(wl.segments), torch.cat([seg_dev[i][0] for i in s.segs]),
-                     torch.cat([seg_dev[i][1] for i in s.segs]))
-    del seg_dev
-    cache.set_tuning(seg_chunks=args.seg, split_chunks=args.split, schedule=args.schedule)
-    rows = cache.seq_order()
-    q = torch.from_numpy(np.ascontiguousarray(wl.q[rows])).cuda()
-    o = torch.empty_like(q)
-    model = call_model(cache.tables(), wl.H, wl.d, 2)
+    wl, cache, q, o, rows, model = static_setup(args.config, args.seg, args.split, args.schedule)
     B = model["B"]
     stats = cache.stats()
-    torch.cuda.synchronize()
 
     def call():
         cache.attention(q, out=o)
@@ -118,23 +106,6 @@ def main():
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     ms_per_step = elapsed * 1e3 / args.steps
-
-    def back_to_back(fn, n):
-        """Mean device time per fn() over n back-to-back launches, with events
-        on the launch stream (no host synchronisation in between). A spin
-        kernel holds the stream while the host enqueues, so a launch that is
-        shorter than the host's per-call cost still runs back to back."""
-        fn()
-        torch.cuda.synchronize()
-        a = torch.cuda.Event(enable_timing=True)
-        b = torch.cuda.Event(enable_timing=True)
-        torch.cuda._sleep(40_000_000)
-        a.record()
-        for _ in range(n):
-            fn()
-        b.record()
-        b.synchronize()
-        return a.elapsed_time(b) * 1e3 / n
 
     n_ev = max(args.steps, 50)
     call_us = back_to_back(call, n_ev)
@@ -156,7 +127,7 @@ def main():
     torch.cuda.synchronize()
 
     tpp_bytes = model["shared_kv"] + model["private_kv"] + model["q"]
-    traffic = counter_traffic(wl.name)
+    traffic, traffic_source = counter_traffic(wl.name)
     tpp_gbps = tpp_bytes / (tpp_us * 1e-6) / 1e9
     ksf_gbps = model["ksf_bytes"] / (ksf_us * 1e-6) / 1e9
     kcf_tflops = model["kcf_flops"] / (kcf_us * 1e-6) / 1e12
@@ -177,6 +148,8 @@ def main():
         "config": {"workload": wl.name, "B": B, "H": wl.H, "d": wl.d, "c": wl.c,
                    "shared_tokens": int(model["shared_kv"] // (2 * wl.H * wl.d * 2)),
                    "private_tokens_per_row": int(model["private_kv"] // (2 * wl.H * wl.d * 2) // B)},
+        "value_kind": "warm: back-to-back calls on one resident tree (its 285.7 MB partly stays in "
+                      "the 256 MB Infinity Cache); see cold for calls after a cache flush",
         "us_per_call": us,
         "us_per_call_events": call_us,
         "algorithmic_bytes_per_call": model["total"],
@@ -186,6 +159,7 @@ def main():
         "roofline": {"bound": "hbm", "kernel": "tpp_kernel (fused chunk-first + sequence-first + merge)",
                      "achieved": tpp_gbps, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                      "frac": tpp_gbps / PEAK_HBM_GBPS, "traffic": traffic,
+                     "traffic_source": traffic_source,
                      "bytes_per_launch": tpp_bytes, "us_per_launch": tpp_us},
         "copy_512MiB": {"us": copy_us, "GBps": copy_bytes / (copy_us * 1e-6) / 1e9},
         "sequence_first_alone": {"kernel": "ksf_kernel", "us_per_launch": ksf_us,
@@ -197,17 +171,97 @@ def main():
                               "GBps": (model["shared_kv"] + model["q"]) / (kcf_us * 1e-6) / 1e9},
     }
     if not args.no_cold:
-        out["cold"] = cold_times(call, cache, model)
+        out["cold"] = cold_times(call, model["total"], model["B"])
+        cache.set_tuning(phase_mask=2)    # the sequence-first kernel alone, same flush
+        ksf_cold = cold_times(call, model["ksf_bytes"], model["B"])
+        cache.set_tuning(phase_mask=7)
+        out["sequence_first_alone"]["cold"] = {k: ksf_cold[k] for k in ("us_per_call", "GBps", "frac")}
     cache.close()
     del cache, q, o
     torch.cuda.empty_cache()
+    if not args.no_other_configs and args.config == 2:
+        out["other_configs"] = {str(c): other_config(c, args.steps, not args.no_cold) for c in (3, 4)}
     if not args.no_dynamic:
         out["dynamic"] = dynamic_run()
     if not args.no_prefill:
         out["prefill"] = prefill_run()
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(wl, rows, args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(wl, rows, args.cpu_seconds, with_dynamic=not args.no_dynamic)
     print(json.dumps(out), flush=True)
+
+
+def static_setup(config, seg=0, split=-1, schedule=-1):
+    """A static workload's tree in a fresh cache, its q in tree row order,
+    an output buffer and the call's byte model; inputs resident on the GPU."""
+    import numpy as np
+    import torch
+
+    from paper_2402_15220_amd.cache import Cache
+    from paper_2402_15220_amd.roofline import call_model
+    from workloads import make_static
+
+    wl = make_static(config)
+    nodes = sum(-(-len(s) // wl.c) for s in wl.segments)
+    cache = Cache(wl.c, wl.H, wl.d, nodes + 16, dtype=torch.float16)
+    seg_dev = [(torch.from_numpy(s.k).cuda(), torch.from_numpy(s.v).cuda()) for s in wl.segments]
+    for s in wl.seqs:
+        cache.insert(s.seq_id, s.tokens(wl.segments), torch.cat([seg_dev[i][0] for i in s.segs]),
+                     torch.cat([seg_dev[i][1] for i in s.segs]))
+    del seg_dev
+    cache.set_tuning(seg_chunks=seg, split_chunks=split, schedule=schedule)
+    rows = cache.seq_order()
+    q = torch.from_numpy(np.ascontiguousarray(wl.q[rows])).cuda()
+    o = torch.empty_like(q)
+    model = call_model(cache.tables(), wl.H, wl.d, 2)
+    torch.cuda.synchronize()
+    return wl, cache, q, o, rows, model
+
+
+def back_to_back(fn, n):
+    """Mean device time per fn() over n back-to-back launches, with events
+    on the launch stream (no host synchronisation in between). A spin
+    kernel holds the stream while the host enqueues, so a launch that is
+    shorter than the host's per-call cost still runs back to back."""
+    import torch
+
+    fn()
+    torch.cuda.synchronize()
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    torch.cuda._sleep(40_000_000)
+    a.record()
+    for _ in range(n):
+        fn()
+    b.record()
+    b.synchronize()
+    return a.elapsed_time(b) * 1e3 / n
+
+
+def other_config(config, n, cold):
+    """Warm (back-to-back) and cold figures of another static workload: the
+    4096-token prompt (3) or the two-level tree of 64 rows (4)."""
+    import torch
+
+    from paper_2402_15220_amd.roofline import PEAK_HBM_GBPS
+
+    wl, cache, q, o, _, model = static_setup(config)
+
+    def call():
+        cache.attention(q, out=o)
+
+    for _ in range(5):
+        call()
+    warm = back_to_back(call, max(n, 50))
+    r = {"workload": wl.name, "B": model["B"], "algorithmic_bytes_per_call": model["total"],
+         "warm": {"us_per_call": warm, "tok_per_s": model["B"] / (warm * 1e-6),
+                  "GBps": model["total"] / (warm * 1e-6) / 1e9,
+                  "frac": model["total"] / (warm * 1e-6) / 1e9 / PEAK_HBM_GBPS}}
+    if cold:
+        r["cold"] = cold_times(call, model["total"], model["B"])
+    cache.close()
+    del cache, q, o
+    torch.cuda.empty_cache()
+    return r
 
 
 def decode_sources_hash(csrc):
@@ -228,28 +282,31 @@ def decode_sources_hash(csrc):
 
 
 def counter_traffic(workload):
-    """HBM bytes per tpp_kernel launch from the committed rocprofv3 counter
-    passes (FETCH_SIZE and WRITE_SIZE scaled by a plain copy), or None when
-    the kernels changed since the counters were taken or the workload
-    differs."""
-    import hashlib
-
-    path = os.path.join(ROOT, "profiles", "tpp_kernel_single_prompt_b32_traffic.json")
+    """HBM bytes per tpp_kernel launch, taken from the committed rocprofv3
+    counter passes (FETCH_SIZE and WRITE_SIZE, each scaled by what it reads
+    for a plain copy of known size); not measured in this run. Returns
+    (bytes or None, source): None when the kernels' code changed since the
+    counters were taken (hash mismatch) or the workload differs."""
+    rel = os.path.join("profiles", "tpp_kernel_single_prompt_b32_traffic.json")
     csrc = os.path.join(ROOT, "paper_2402_15220_amd", "csrc")
+    sha = decode_sources_hash(csrc)
+    src = {"taken_from": rel, "measured_in_this_run": False, "decode_sources_sha256_16": sha}
     try:
-        with open(path) as f:
+        with open(os.path.join(ROOT, rel)) as f:
             rec = json.load(f)
-        sha = decode_sources_hash(csrc)
     except OSError:
-        return None
-    if rec.get("decode_sources_sha256_16") != sha or rec.get("workload") != workload:
-        return None
-    return rec["kernels"]["tpp_kernel"]["traffic_bytes"]
+        return None, dict(src, status="no counter record")
+    if rec.get("decode_sources_sha256_16") != sha:
+        return None, dict(src, status="stale: kernels changed since the counters were taken")
+    if rec.get("workload") != workload:
+        return None, dict(src, status="counters are for another workload")
+    return rec["kernels"]["tpp_kernel"]["traffic_bytes"], dict(src, status="current")
 
 
-def cold_times(call, cache, model, n=30):
+def cold_times(call, nbytes, rows, n=30):
     """Median device time per call after a clean (read-only) 1 GiB pass that
-    evicts L2 and the 256 MB Infinity Cache, events around the call only."""
+    evicts L2 and the 256 MB Infinity Cache, events around the call only;
+    rates for `nbytes` algorithmic bytes and `rows` tokens per call."""
     import numpy as np
     import torch
 
@@ -267,8 +324,8 @@ def cold_times(call, cache, model, n=30):
     us = float(np.median([a.elapsed_time(b) * 1e3 for a, b in evs]))
     from paper_2402_15220_amd.roofline import PEAK_HBM_GBPS
 
-    gbps = model["total"] / (us * 1e-6) / 1e9
-    return {"us_per_call": us, "tok_per_s": model["B"] / (us * 1e-6), "GBps": gbps,
+    gbps = nbytes / (us * 1e-6) / 1e9
+    return {"us_per_call": us, "tok_per_s": rows / (us * 1e-6), "GBps": gbps,
             "frac": gbps / PEAK_HBM_GBPS, "calls": n,
             "flush": "clean 1 GiB read between calls; median of per-call event pairs "
                      "(each pair adds ~2 us of marker overhead)"}
@@ -460,32 +517,124 @@ def dynamic_run():
             **pipe}
 
 
-def cpu_baseline(wl, rows, seconds):
-    """The oracle (float64 NumPy) on the same tree and queries, timed on the
-    host. Sample: whole calls (all B rows, all heads), repeated until about
-    `seconds` of CPU time; tree construction is not timed."""
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
     import platform
 
-    from oracle import OracleTree, dense_attention_rows
+    return platform.processor() or platform.machine()
 
+
+def _oracle_rows(tree, row_seq, q, scale, rows, pool, threads):
+    """The oracle's dense_attention_rows over `rows`, split into groups that
+    run on a thread pool (NumPy releases the GIL in its copies and
+    reductions); the oracle itself is unchanged."""
+    import numpy as np
+
+    from oracle import dense_attention_rows
+
+    rows = list(rows)
+    if threads <= 1:
+        return dense_attention_rows(tree, row_seq, q, scale, rows=rows)
+    per = -(-len(rows) // threads)
+    groups = [rows[i:i + per] for i in range(0, len(rows), per)]
+    return np.concatenate(list(pool.map(
+        lambda g: dense_attention_rows(tree, row_seq, q, scale, rows=g), groups)))
+
+
+def cpu_baseline(wl, rows, seconds, with_dynamic=True):
+    """The oracle (float64 NumPy, as written) timed on the host: whole calls
+    of the bench workload (all B rows, all heads) with the rows split over
+    one thread per host CPU (at most 16, the GPU's host share), repeated for
+    about `seconds`; one single-threaded call; the oracle's tree operations
+    (building the bench tree); and, on the 64-step decode workload, the
+    oracle's per-step tree operations and attention for a sample of steps."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    from oracle import OracleTree
+
+    threads = max(1, min(16, len(os.sched_getaffinity(0))))
     t = OracleTree(c=wl.c)
+    t0 = time.perf_counter()
     for s in wl.seqs:
         k, v = s.kv(wl.segments)
         t.insert(s.seq_id, s.tokens(wl.segments), k, v)
+    tree_build_s = time.perf_counter() - t0
     q = wl.q[rows]
-    n = 0
+    with ThreadPoolExecutor(threads) as pool:
+        _oracle_rows(t, rows, q, wl.scale, range(len(rows)), pool, threads)   # warm-up
+        n = 0
+        t0 = time.perf_counter()
+        while True:
+            _oracle_rows(t, rows, q, wl.scale, range(len(rows)), pool, threads)
+            n += 1
+            if time.perf_counter() - t0 >= seconds:
+                break
+        el = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        _oracle_rows(t, rows, q, wl.scale, range(len(rows)), pool, 1)
+        single_s = time.perf_counter() - t0
+        dyn = dynamic_oracle_sample(pool, threads) if with_dynamic else None
+    out = {"value": n * len(rows) / el, "unit": "tok/s", "cores": threads, "kind": "oracle",
+           "sample": f"{n} full calls of the workload (B={len(rows)} rows x {wl.H} heads, float64 "
+                     f"NumPy, rows split over {threads} threads), after one untimed call",
+           "ms_per_call": el * 1e3 / n, "cpu": _cpu_model(),
+           "host_cpus": len(os.sched_getaffinity(0)),
+           "single_thread": {"ms_per_call": single_s * 1e3, "tok_per_s": len(rows) / single_s},
+           "tree_ops": {"what": f"building the bench tree: {len(wl.seqs)} inserts with K/V rows",
+                        "ms": tree_build_s * 1e3}}
+    if dyn is not None:
+        out["dynamic"] = dyn
+    return out
+
+
+def dynamic_oracle_sample(pool, threads, sample_steps=(0, 16)):
+    """The oracle on the 64-step decode workload: its tree is built (timed
+    as tree operations), then it runs the steps in order (churn, one append
+    per row), timing each step's tree operations; at the sampled steps it
+    also computes the step's attention for every row."""
+    import numpy as np
+
+    from oracle import OracleTree
+    from workloads import make_dynamic
+
+    wl = make_dynamic()
+    t = OracleTree(c=wl.c)
     t0 = time.perf_counter()
-    while True:
-        dense_attention_rows(t, rows, q, wl.scale)
-        n += 1
-        if time.perf_counter() - t0 >= seconds:
+    for s in wl.seqs:
+        k, v = s.kv(wl.segments)
+        t.insert(s.seq_id, s.tokens(wl.segments), k, v)
+    build_s = time.perf_counter() - t0
+    ops_s, att_s = [], []
+    last = max(sample_steps)
+    for st in wl.steps():
+        t0 = time.perf_counter()
+        if st.churn:
+            for sid in st.churn.removed:
+                t.remove(sid)
+            for s in st.churn.added:
+                k, v = s.kv(wl.segments)
+                t.insert(s.seq_id, s.tokens(wl.segments), k, v)
+        t.append_batch(st.live, st.tokens, st.k, st.v)
+        ops_s.append(time.perf_counter() - t0)
+        if st.step in sample_steps:
+            # rows in the caller's (sorted id) order: the result does not depend on it
+            t0 = time.perf_counter()
+            _oracle_rows(t, st.live, st.q, wl.scale, range(len(st.live)), pool, threads)
+            att_s.append(time.perf_counter() - t0)
+        if st.step >= last:
             break
-    el = time.perf_counter() - t0
-    return {"value": n * len(rows) / el, "unit": "tok/s", "cores": 1, "kind": "oracle",
-            "sample": f"{n} full calls of the workload (B={len(rows)} rows x {wl.H} heads, "
-                      f"float64 NumPy einsum, single-threaded)",
-            "ms_per_call": el * 1e3 / n, "host_cpus": len(os.sched_getaffinity(0)),
-            "cpu": platform.processor() or platform.machine()}
+    return {"workload": wl.name, "initial_tree_build_ms": build_s * 1e3,
+            "tree_ops_ms_per_step_mean": float(np.mean(ops_s)) * 1e3,
+            "tree_ops_steps_timed": len(ops_s),
+            "attention_ms_per_step": [a * 1e3 for a in att_s],
+            "attention_steps": list(sample_steps), "threads": threads,
+            "tok_per_s": len(st.live) * len(att_s) / sum(att_s)}
 
 
 if __name__ == "__main__":
