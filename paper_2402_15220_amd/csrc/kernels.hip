@@ -140,6 +140,82 @@ __device__ __forceinline__ void fold_parts(int k0, int k1, const int32_t* parts,
   }
 }
 
+// fold_parts for at most 64 partials whose indices are already in lanes
+// (lane k holds the k-th, pidx < 0 past the end): the maxima and every
+// partial O vector are requested together, one round trip instead of a
+// chain of index, maximum and vector loads, then folded (Eqn 2) with one
+// common maximum. Same lane layout, arguments and result as fold_parts.
+template <int E, int G, bool DEV>
+__device__ __forceinline__ void fold_parts_lanes(int pidx, const float* ws_o, uint32_t o_bytes,
+                                                 const float2* ws_ml, int H, int D, int h, int d0,
+                                                 int lane, float& m, float& n, float* acc, int skip) {
+  constexpr int NB = 32 / E;  // partials per group per pass
+  static_assert(E % 4 == 0 && NB >= 1 && G >= 1 && 64 % G == 0, "fold layout");
+  const int gi = lane / (64 / G);
+  const bool valid = pidx >= 0 && pidx != skip;
+  const unsigned long long vm = __ballot(valid);
+  if (vm == 0) return;  // uniform: nothing to fold
+  // an absent or skipped partial reads a valid one in its place (weight 0)
+  const int ps = valid ? pidx : __builtin_amdgcn_readlane(pidx, __builtin_ctzll(vm));
+  const __amdgpu_buffer_rsrc_t rs = part_rsrc(ws_o, o_bytes);
+  float pm = kNegBig, pn = 0.f;
+  if (valid) {
+    const float* ml = reinterpret_cast<const float*>(ws_ml + static_cast<size_t>(ps) * H + h);
+    if constexpr (DEV) {
+      pm = ld_dev(ml);
+      pn = ld_dev(ml + 1);
+    } else {
+      pm = ml[0];
+      pn = ml[1];
+    }
+  }
+  const int kend = 64 - __builtin_clzll(vm);  // one past the last valid lane
+  auto load_pass = [&](int kb, float (*x)[E]) {
+#pragma unroll
+    for (int u = 0; u < NB; ++u) {
+      const int kc = min(kb + G * u + gi, 63);
+      const int pk = __shfl(ps, kc);
+#pragma unroll
+      for (int j = 0; j < E; j += 4) {
+        float4 v;
+        if constexpr (DEV) {
+          v = ld_dev4(rs, part_off(pk, H, D, h, d0 + j));
+        } else {
+          v = *reinterpret_cast<const float4*>(ws_o + (static_cast<size_t>(pk) * H + h) * D + d0 + j);
+        }
+        x[u][j] = v.x;
+        x[u][j + 1] = v.y;
+        x[u][j + 2] = v.z;
+        x[u][j + 3] = v.w;
+      }
+    }
+  };
+  float x[NB][E];
+  load_pass(0, x);  // in flight with the maxima
+  const float M = fmaxf(m, wave_max(pm));
+  const float wself = fast_exp2(m - M);
+  const float wp = valid ? fast_exp2(pm - M) : 0.f;
+  n = n * wself + wave_sum(wp * pn);
+#pragma unroll
+  for (int j = 0; j < E; ++j) acc[j] = gi == 0 ? acc[j] * wself : 0.f;
+  for (int kb = 0; kb < kend; kb += NB * G) {
+    if (kb > 0) load_pass(kb, x);
+#pragma unroll
+    for (int u = 0; u < NB; ++u) {
+      const int k = kb + G * u + gi;
+      const float wk = k < 64 ? __shfl(wp, min(k, 63)) : 0.f;
+#pragma unroll
+      for (int j = 0; j < E; ++j) acc[j] = fmaf(wk, x[u][j], acc[j]);
+    }
+  }
+  m = M;
+#pragma unroll
+  for (int j = 0; j < E; ++j) {
+#pragma unroll
+    for (int off = 64 / G; off < 64; off <<= 1) acc[j] += __shfl_xor(acc[j], off);
+  }
+}
+
 // Finish row `row`, head h from its partials (Eqn 2, then O/n) and write o.
 // One wavefront; lanes [0, D/4) own four consecutive d each. DEV selects
 // device-scope loads (partials written by other blocks of the same launch).
@@ -206,22 +282,19 @@ __device__ __forceinline__ void ksf_block(const KsfParams& P, int item, int h, c
   constexpr int U = 64 / TPS;
   static_assert(U >= 1 && TPS * U == 64, "step must cover 64 tokens");
 
-  const SfItem it = P.items[item];
   const int H = P.H, C = P.C;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int sub = lane % LPT, tr = lane / LPT;
 
-  float qf[EPL];
-  {
-    const uint4 qr = *reinterpret_cast<const uint4*>(static_cast<const T*>(P.q) +
-                                                     (static_cast<size_t>(io_row(P.row_map, it.row)) * H + h) * D +
-                                                     sub * EPL);
-    E::unpack(qr, qf);
-  }
-
-  float m = kNegBig, n = 0.f, acc[EPL];
-#pragma unroll
-  for (int j = 0; j < EPL; ++j) acc[j] = 0.f;
+  // Everything the stream needs first is requested in the first round trip
+  // or right after it: the item record (uniform) and, from the record's
+  // inline copy, the slots of the first kSfInline chunks (one per lane);
+  // then the first step's K/V rows, the first chunk's length, q, the row's
+  // partial indices and the other lanes' lengths. No load waits on a chain
+  // of other loads before the stream starts.
+  const SfItem* itp = P.items + item;
+  const SfItem it = *itp;
+  int slot_lo = lane < kSfInline ? itp->slot[lane] : 0;
 
   const T* kpool = static_cast<const T*>(P.kpool) + h * P.hs + sub * EPL;
   const T* vpool = static_cast<const T*>(P.vpool) + h * P.hs + sub * EPL;
@@ -249,13 +322,40 @@ __device__ __forceinline__ void ksf_block(const KsfParams& P, int item, int h, c
           uint4, __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(vb + row)));
     }
   };
+
+  const int n_chunks = it.ce - it.cb;
+  const int cm = min(C, 64);  // rows of a chunk's first step when the chunk is full
+  uint4 kr[U], vr[U];
+  // The first step of the first chunk goes out before the chunk's length
+  // is known, as if the chunk were full (rows clamped to the tile, so in
+  // bounds); a shorter chunk is requested again with the right clamp below
+  // (rows past its length may hold anything, even NaN, and are never used).
+  if (n_chunks > 0) load_step(kr, vr, it.slot[0], 0, cm);
+  const int gn0 = min(64, n_chunks);
+  int slot_hi = 0;
+  if (lane >= it.n_inline && lane < gn0) slot_hi = P.priv_slot[it.cb + lane];
+  const uint4 qr = *reinterpret_cast<const uint4*>(static_cast<const T*>(P.q) +
+                                                   (static_cast<size_t>(io_row(P.row_map, it.row)) * H + h) * D +
+                                                   sub * EPL);
+  const int np = it.part_e - it.part_b;
+  int pidx = -1;
+  if (w == 0 && lane < np && np <= 64) pidx = P.parts[it.part_b + lane];
+  const int len0 = n_chunks > 0 ? P.slot_len[it.slot[0]] : 0;
+  int len_lo = lane < it.n_inline ? P.slot_len[slot_lo] : 0;
+  float qf[EPL];
+  E::unpack(qr, qf);
+
+  float m = kNegBig, n = 0.f, acc[EPL];
+#pragma unroll
+  for (int j = 0; j < EPL; ++j) acc[j] = 0.f;
+
   // online softmax over one 64-token step (Eqn 1 for the step, folded by Eqn 2)
-  auto do_step = [&](const uint4* kr, const uint4* vr, int t0, int len) {
+  auto do_step = [&](const uint4* kr_, const uint4* vr_, int t0, int len) {
     float s[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       float kf[EPL];
-      E::unpack(kr[u], kf);
+      E::unpack(kr_[u], kf);
       float dot = 0.f;
 #pragma unroll
       for (int j = 0; j < EPL; ++j) dot = fmaf(qf[j], kf[j], dot);
@@ -278,30 +378,50 @@ __device__ __forceinline__ void ksf_block(const KsfParams& P, int item, int h, c
       const float p = fast_exp2(s[u] - mn);
       n += p;
       float vf[EPL];
-      E::unpack(vr[u], vf);
+      E::unpack(vr_[u], vf);
 #pragma unroll
       for (int j = 0; j < EPL; ++j) acc[j] = fmaf(p, vf[j], acc[j]);
     }
     m = mn;
   };
 
-  // Chunks are taken 64 at a time: lane i holds the slot and length of chunk
-  // i of the group, broadcast with readlane (no dependent metadata loads in
-  // the streaming loop).
-  for (int g0 = it.cb; g0 < it.ce; g0 += 64) {
-    const int gn = min(64, it.ce - g0);
-    int my_slot = 0, my_len = 0;
-    if (lane < gn) {
-      my_slot = P.priv_slot[g0 + lane];
-      my_len = P.slot_len[my_slot];
+  if (n_chunks > 0) {
+    // chunks are taken 64 at a time: lane i holds the slot and length of
+    // chunk i of the group, broadcast with readlane; in the first group the
+    // first kSfInline come from the record (slot_lo, len_lo) and the others
+    // from priv_slot (slot_hi, len_hi), so the early chunks never wait for
+    // the later ones' lengths
+    if (len0 < cm) load_step(kr, vr, it.slot[0], 0, len0);  // uniform; rare
+    do_step(kr, vr, 0, len0);
+    int len_hi = 0;
+    if (lane >= it.n_inline && lane < gn0) len_hi = P.slot_len[slot_hi];
+    int jj = 0, t0 = 64, len = len0, slot = it.slot[0];
+    while (true) {
+      if (t0 >= len) {
+        if (++jj >= gn0) break;
+        const bool lo = jj < it.n_inline;
+        slot = __builtin_amdgcn_readlane(lo ? slot_lo : slot_hi, jj);
+        len = __builtin_amdgcn_readlane(lo ? len_lo : len_hi, jj);
+        t0 = 0;
+      }
+      load_step(kr, vr, slot, t0, len);
+      do_step(kr, vr, t0, len);
+      t0 += 64;
     }
-    for (int jj = 0; jj < gn; ++jj) {
-      const int slot = __builtin_amdgcn_readlane(my_slot, jj);
-      const int len = __builtin_amdgcn_readlane(my_len, jj);
-      for (int t0 = 0; t0 < len; t0 += 64) {
-        uint4 kr[U], vr[U];
-        load_step(kr, vr, slot, t0, len);
-        do_step(kr, vr, t0, len);
+    for (int g0 = it.cb + 64; g0 < it.ce; g0 += 64) {
+      const int gn = min(64, it.ce - g0);
+      int my_slot = 0, my_len = 0;
+      if (lane < gn) {
+        my_slot = P.priv_slot[g0 + lane];
+        my_len = P.slot_len[my_slot];
+      }
+      for (int j = 0; j < gn; ++j) {
+        const int sl = __builtin_amdgcn_readlane(my_slot, j);
+        const int ln = __builtin_amdgcn_readlane(my_len, j);
+        for (int tt = 0; tt < ln; tt += 64) {
+          load_step(kr, vr, sl, tt, ln);
+          do_step(kr, vr, tt, ln);
+        }
       }
     }
   }
@@ -330,70 +450,70 @@ __device__ __forceinline__ void ksf_block(const KsfParams& P, int item, int h, c
 #pragma unroll
   for (int ww = 1; ww < 4; ++ww) fold<EPL>(m, n, acc, st[ww][sub][0], st[ww][sub][1], &st[ww][sub][2]);
 
-  if (it.out_part < 0) {
-    // fold the row's chunk-first partials (Algorithm 2), then O/n
-    fold_parts<EPL, 64 / LPT, false>(P.part_ptr[it.row], P.part_ptr[it.row + 1], P.parts, P.ws_o,
-                                     P.o_bytes, P.ws_ml, H, D, h, sub * EPL, lane, m, n, acc);
+  auto write_o = [&]() {
     if (tr != 0) return;
     const float inv = 1.f / n;
 #pragma unroll
     for (int j = 0; j < EPL; ++j) acc[j] *= inv;
     *reinterpret_cast<uint4*>(static_cast<T*>(P.o) + (static_cast<size_t>(io_row(P.row_map, it.row)) * H + h) * D +
                               sub * EPL) = E::pack(acc);
-  } else {
-    if (P.cnt) {
-      // If every other contributor of the row has already arrived (the usual
-      // case: chunk-first items are dispatched first), fold their partials
-      // straight into this item's state and finish the row: no partial, no
-      // arrival. The counter goes back to zero. This relies on the exchange
-      // protocol of device_common.hpp: a count of need - 1, read with a
-      // device-scope load, means every other part was visible before it was
-      // counted; the branch on it precedes every part load (the compiler
-      // fence keeps them there) and those loads are device-scope (fold_parts
-      // with DEV = true).
-      const int k0 = P.part_ptr[it.row], k1 = P.part_ptr[it.row + 1];
-      int32_t* c = P.cnt + static_cast<size_t>(it.row) * H + h;
-      int ready = 0;
-      if (lane == 0)
-        ready = __hip_atomic_load(c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == k1 - k0 - 1;
-      if (__shfl(ready, 0)) {
-        compiler_fence();
-        fold_parts<EPL, 64 / LPT, true>(k0, k1, P.parts, P.ws_o, P.o_bytes, P.ws_ml, H, D, h,
-                                        sub * EPL, lane, m, n, acc, it.out_part);
-        if (lane == 0) __hip_atomic_store(c, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (tr != 0) return;
-        const float inv = 1.f / n;
+  };
+  if (it.out_part < 0) {
+    // fold the row's chunk-first partials (Algorithm 2), then O/n
+    if (np <= 64)
+      fold_parts_lanes<EPL, 64 / LPT, false>(pidx, P.ws_o, P.o_bytes, P.ws_ml, H, D, h, sub * EPL,
+                                             lane, m, n, acc, -1);
+    else
+      fold_parts<EPL, 64 / LPT, false>(it.part_b, it.part_e, P.parts, P.ws_o, P.o_bytes, P.ws_ml, H,
+                                       D, h, sub * EPL, lane, m, n, acc);
+    write_o();
+    return;
+  }
+  if (P.cnt) {
+    // If every other contributor of the row has already arrived (the usual
+    // case: chunk-first items are dispatched first), fold their partials
+    // straight into this item's state and finish the row: no partial, no
+    // arrival. The counter goes back to zero. This relies on the exchange
+    // protocol of device_common.hpp: a count of need - 1, read with a
+    // device-scope load, means every other part was visible before it was
+    // counted; the branch on it precedes every part load (the compiler
+    // fence keeps them there) and those loads are device-scope (DEV = true).
+    int32_t* c = P.cnt + static_cast<size_t>(it.row) * H + h;
+    int ready = 0;
+    if (lane == 0) ready = __hip_atomic_load(c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == np - 1;
+    if (__shfl(ready, 0)) {
+      compiler_fence();
+      if (np <= 64)
+        fold_parts_lanes<EPL, 64 / LPT, true>(pidx, P.ws_o, P.o_bytes, P.ws_ml, H, D, h, sub * EPL,
+                                              lane, m, n, acc, it.out_part);
+      else
+        fold_parts<EPL, 64 / LPT, true>(it.part_b, it.part_e, P.parts, P.ws_o, P.o_bytes, P.ws_ml, H,
+                                        D, h, sub * EPL, lane, m, n, acc, it.out_part);
+      if (lane == 0) __hip_atomic_store(c, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      write_o();
+      return;
+    }
+  }
+  if (tr == 0) {
+    const __amdgpu_buffer_rsrc_t rs = part_rsrc(P.ws_o, P.o_bytes);
 #pragma unroll
-        for (int j = 0; j < EPL; ++j) acc[j] *= inv;
-        *reinterpret_cast<uint4*>(static_cast<T*>(P.o) + (static_cast<size_t>(io_row(P.row_map, it.row)) * H + h) * D +
-                                  sub * EPL) = E::pack(acc);
-        return;
-      }
+    for (int j = 0; j < EPL; j += 4)
+      st_dev4(rs, part_off(it.out_part, H, D, h, sub * EPL + j), acc[j], acc[j + 1], acc[j + 2],
+              acc[j + 3]);
+    if (sub == 0) {
+      float* pml = reinterpret_cast<float*>(P.ws_ml + static_cast<size_t>(it.out_part) * H + h);
+      st_dev(pml, m);
+      st_dev(pml + 1, n);
     }
-    if (tr == 0) {
-      const __amdgpu_buffer_rsrc_t rs = part_rsrc(P.ws_o, P.o_bytes);
-#pragma unroll
-      for (int j = 0; j < EPL; j += 4)
-        st_dev4(rs, part_off(it.out_part, H, D, h, sub * EPL + j), acc[j], acc[j + 1], acc[j + 2],
-                acc[j + 3]);
-      if (sub == 0) {
-        float* pml = reinterpret_cast<float*>(P.ws_ml + static_cast<size_t>(it.out_part) * H + h);
-        st_dev(pml, m);
-        st_dev(pml + 1, n);
-      }
-    }
-    if (P.cnt) {
-      // partial-writing schedules: the last contributor of the row finishes it
-      wait_stores();
-      int last = 0;
-      if (lane == 0) {
-        const int need = P.part_ptr[it.row + 1] - P.part_ptr[it.row];
-        last = arrive_last(P.cnt + static_cast<size_t>(it.row) * H + h, need);
-      }
-      if (__shfl(last, 0))
-        finish_row<T, D, true>(P.part_ptr, P.parts, P.ws_o, P.o_bytes, P.ws_ml, P.o, P.row_map, H, it.row, h,
-                               lane);
-    }
+  }
+  if (P.cnt) {
+    // partial-writing schedules: the last contributor of the row finishes it
+    wait_stores();
+    int last = 0;
+    if (lane == 0) last = arrive_last(P.cnt + static_cast<size_t>(it.row) * H + h, np);
+    if (__shfl(last, 0))
+      finish_row<T, D, true>(P.part_ptr, P.parts, P.ws_o, P.o_bytes, P.ws_ml, P.o, P.row_map, H, it.row, h,
+                             lane);
   }
 }
 
@@ -1019,7 +1139,6 @@ struct TppParams {
   KsfParams sf;
   int n_cf;        // chunk-first blocks: n_segs * zb * H
   int zb;          // row blocks per segment
-  int block_base;  // first block index of this launch
 };
 
 template <typename T, int D, int NRT>
@@ -1032,7 +1151,7 @@ constexpr int tpp_lds_bytes() {
 template <typename T, int D, int NRT>
 __global__ __launch_bounds__(256, 4) void tpp_kernel(TppParams P) {
   __shared__ __attribute__((aligned(16))) char lds[tpp_lds_bytes<T, D, NRT>()];
-  const int b = static_cast<int>(blockIdx.x) + P.block_base;
+  const int b = static_cast<int>(blockIdx.x);
   const int H = P.sf.H;
   if (b < P.n_cf) {
     const int h = b % H;
@@ -1144,7 +1263,6 @@ hipError_t launch_all(const AttnArgs& a, const DevWork& w, hipStream_t s, int ma
   const int nrt = rows <= 16 || fused ? 1 : 2;
   P.zb = rows > 0 ? (rows + 16 * nrt - 1) / (16 * nrt) : 1;
   P.n_cf = w.n_segs * P.zb * a.H;
-  P.block_base = 0;
   const int n_sf = w.n_items * a.H;
   hipError_t e;
   if (nrt == 1) e = launch_phases<T, D, 1>(P, n_sf, w.schedule, mask, s, side, w.seg_group_ptr, w.n_seg_groups);

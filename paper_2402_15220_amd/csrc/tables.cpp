@@ -6,6 +6,17 @@
 
 namespace ca {
 
+void fill_item_records(WorkLists* w) {
+  WorkLists& W = *w;
+  for (SfItem& it : W.items) {
+    it.part_b = W.part_ptr[it.row];
+    it.part_e = W.part_ptr[it.row + 1];
+    it.n_inline = std::min(it.ce - it.cb, kSfInline);
+    it.pad = 0;
+    for (int i = 0; i < kSfInline; ++i) it.slot[i] = i < it.n_inline ? W.priv_slot[it.cb + i] : 0;
+  }
+}
+
 void build_tables(const ChunkTree& tree, Tables* out) {
   Tables& T = *out;
   const auto& nodes = tree.nodes();
@@ -207,14 +218,14 @@ void build_work(const ChunkTree& tree, const Tables& T, int32_t seg_chunks, int3
     const bool has_shared = static_cast<int32_t>(W.parts.size()) > W.part_ptr.back();
     if (!(partial_items && has_shared) && (split_chunks <= 0 || np <= split_chunks)) {
       // the row's own item produces its output directly
-      W.items.push_back({static_cast<int32_t>(r), pb, pe, -1});
+      W.items.push_back(SfItem{static_cast<int32_t>(r), pb, pe, -1, 0, 0, 0, 0, {}});
     } else {
       // chunk-first partials and/or several private pieces: every piece
       // writes a partial and the merge epilogue produces the output
       const int32_t piece = split_chunks > 0 ? split_chunks : std::max(np, 1);
       for (int32_t c0 = pb; c0 < pe; c0 += piece) {
         const int32_t c1 = std::min(pe, c0 + piece);
-        W.items.push_back({static_cast<int32_t>(r), c0, c1, part});
+        W.items.push_back(SfItem{static_cast<int32_t>(r), c0, c1, part, 0, 0, 0, 0, {}});
         W.parts.push_back(part);
         ++part;
       }
@@ -265,6 +276,7 @@ void build_work(const ChunkTree& tree, const Tables& T, int32_t seg_chunks, int3
     W.segs.swap(sorted);
     W.n_parts = B;
   }
+  fill_item_records(&W);
   W.row_of_seq.clear();
   for (int64_t r = 0; r < B; ++r) W.row_of_seq[T.row_seq[r]] = static_cast<int32_t>(r);
   W.item_of_row.assign(B, -1);
@@ -305,6 +317,7 @@ bool patch_work(const ChunkTree& tree, WorkLists* w) {
   for (size_t i = 0; i < order.size(); ++i) sorted[i] = W.items[order[i]];
   W.items.swap(sorted);
   for (size_t i = 0; i < W.items.size(); ++i) W.item_of_row[W.items[i].row] = static_cast<int32_t>(i);
+  fill_item_records(&W);
   return true;
 }
 
@@ -329,6 +342,14 @@ const char* same_work(const WorkLists& a, const WorkLists& b) {
     return k;
   };
   if (key(a) != key(b)) return "sequence-first items";
+  for (const WorkLists* w : {&a, &b})
+    for (const auto& it : w->items) {
+      if (it.part_b != w->part_ptr[it.row] || it.part_e != w->part_ptr[it.row + 1] ||
+          it.n_inline != std::min(it.ce - it.cb, kSfInline))
+        return "item records";
+      for (int i = 0; i < it.n_inline; ++i)
+        if (it.slot[i] != w->priv_slot[it.cb + i]) return "item records";
+    }
   return "";
 }
 

@@ -73,6 +73,9 @@ struct WorkLists {
 // fold (not the first on their rows' paths).
 // token_head_bytes: K+V bytes of one token of one head (2·d·element size),
 // used by the automatic segment size to estimate the sequence-first stream.
+// The derived fields of every item record (partial range, inline slots).
+void fill_item_records(WorkLists* w);
+
 void build_work(const ChunkTree& tree, const Tables& t, int32_t seg_chunks, int32_t split_chunks,
                 bool partial_items, int32_t num_heads, int32_t num_cus, WorkLists* out,
                 bool serial_reduce = false, int32_t token_head_bytes = 512);

@@ -20,15 +20,25 @@ struct CfSeg {
 
 // A sequence-first item: row `row`, private chunks priv_slot[cb, ce).
 // out_part < 0: the item owns the row's result; it merges the row's segment
-// partials and writes o. Otherwise it writes partial out_part.
+// partials and writes o. Otherwise it writes partial out_part. The record
+// also carries what the item's block would otherwise fetch through chains
+// of dependent loads: the row's partial list parts[part_b, part_e) and the
+// slots of its first kSfInline private chunks (slot[i] = priv_slot[cb + i]
+// for i < n_inline = min(ce - cb, kSfInline)).
+constexpr int kSfInline = 8;
 struct SfItem {
   int32_t row;
   int32_t cb;
   int32_t ce;
   int32_t out_part;
+  int32_t part_b;
+  int32_t part_e;
+  int32_t n_inline;
+  int32_t pad;
+  int32_t slot[kSfInline];
 };
 
 static_assert(sizeof(CfSeg) == 32, "CfSeg layout");
-static_assert(sizeof(SfItem) == 16, "SfItem layout");
+static_assert(sizeof(SfItem) == 64, "SfItem layout");
 
 }  // namespace ca
