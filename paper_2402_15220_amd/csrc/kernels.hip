@@ -563,6 +563,7 @@ struct KcfParams {
   const int32_t* part_ptr;
   const int32_t* parts;
   const int32_t* row_map;  // tree row -> row of q and o (null: tree order)
+  int seg_base = 0;        // index in the whole segment list of segs[0]
 };
 
 // Partial-writing schedules: after a chunk-first block wrote its partials for rows
@@ -646,7 +647,10 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
   float* mbuf = reinterpret_cast<float*>(lds + BIG);  // [4][R]
   float* nbuf = mbuf + 4 * R;                         // [4][R]
 
+  // The segment's slots sit at a fixed stride, so they are requested with
+  // the segment record, in the same round trip (one per lane).
   const CfSeg sg = P.segs[seg];
+  const int my_slot = P.seg_slots[(P.seg_base + seg) * kSegSlotStride + lane];
   const int H = P.H, C = P.C;
   const int rb = sg.row_begin + z * R;
   const int nrows = min(R, sg.row_end - rb);
@@ -682,11 +686,7 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
   }
 
   // Segment chunks (at most 64): lane j holds chunk j's slot and length.
-  int my_slot = 0, my_len = 0;
-  if (lane < sg.n_chunks) {
-    my_slot = P.seg_slots[sg.slot_off + lane];
-    my_len = P.slot_len[my_slot];
-  }
+  const int my_len = lane < sg.n_chunks ? P.slot_len[my_slot] : 0;
   // Software pipeline without extra registers: the next block's K rows are
   // requested as soon as this block's S^T MFMAs have read theirs, and its V
   // rows as soon as this block's V rows are in LDS, so each block's loads
@@ -715,11 +715,20 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
                                               (lane % GPR) * 8);
     }
   };
+  // The first block's rows go out before the first chunk's length is
+  // known, as if it were full (rows clamped to the tile: in bounds); a
+  // shorter chunk is requested again with the right clamp (rows past its
+  // length may hold anything, even NaN, and are never used).
   int j = 0, t0 = 0;
   int slot = __builtin_amdgcn_readlane(my_slot, 0);
+  const int cm = min(C, 64);
+  load_k(slot, 0, cm);
+  load_v(slot, 0, cm);
   int len = __builtin_amdgcn_readlane(my_len, 0);
-  load_k(slot, t0, len);
-  load_v(slot, t0, len);
+  if (len < cm) {  // uniform; rare
+    load_k(slot, 0, len);
+    load_v(slot, 0, len);
+  }
   while (true) {
     const int nt = min(64, len - t0);
     // the block after this one; after the last block, the loads re-read one
@@ -1230,6 +1239,7 @@ hipError_t launch_phases(const TppParams& P, int n_sf, int schedule, int mask, h
       for (int gi = 0; gi < n_groups; ++gi) {
         KcfParams g = cf;
         g.segs = cf.segs + group_ptr[gi];
+        g.seg_base = group_ptr[gi];
         const int nb = (group_ptr[gi + 1] - group_ptr[gi]) * P.zb * cf.H;
         if (nb > 0) kcf_kernel<T, D, NRT><<<nb, 256, 0, s>>>(g, P.zb);
       }

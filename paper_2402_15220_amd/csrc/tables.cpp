@@ -276,6 +276,17 @@ void build_work(const ChunkTree& tree, const Tables& T, int32_t seg_chunks, int3
     W.segs.swap(sorted);
     W.n_parts = B;
   }
+  // fixed-stride slot lists: segment i's at i * kSegSlotStride
+  {
+    std::vector<int32_t> packed(W.segs.size() * kSegSlotStride);
+    for (size_t i = 0; i < W.segs.size(); ++i) {
+      CfSeg& sg = W.segs[i];
+      for (int k = 0; k < kSegSlotStride; ++k)
+        packed[i * kSegSlotStride + k] = W.seg_slots[sg.slot_off + std::min(k, sg.n_chunks - 1)];
+      sg.slot_off = static_cast<int32_t>(i * kSegSlotStride);
+    }
+    W.seg_slots.swap(packed);
+  }
   fill_item_records(&W);
   W.row_of_seq.clear();
   for (int64_t r = 0; r < B; ++r) W.row_of_seq[T.row_seq[r]] = static_cast<int32_t>(r);

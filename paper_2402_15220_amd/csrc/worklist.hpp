@@ -6,9 +6,13 @@
 
 namespace ca {
 
-// A chunk-first segment: n_chunks consecutive shared chunks of one run
-// (slots at seg_slots[slot_off ...], root -> leaf) covering query rows
+// A chunk-first segment: n_chunks (<= 64) consecutive shared chunks of one
+// run (slots at seg_slots[slot_off ...], root -> leaf) covering query rows
 // [row_begin, row_end). Partial for row r is part_base + r - row_begin.
+// Segment i's slots start at slot_off = i * kSegSlotStride (padded with its
+// last slot), so a block can request them from its segment index alone,
+// without waiting for the record.
+constexpr int kSegSlotStride = 64;
 struct CfSeg {
   int32_t slot_off;
   int32_t n_chunks;
