@@ -566,33 +566,117 @@ struct KcfParams {
   int seg_base = 0;        // index in the whole segment list of segs[0]
 };
 
-// Partial-writing schedules: after a chunk-first block wrote its partials for rows
-// [rb, rb+nrows), count its arrival on each row; rows for which it is the
-// last contributor are finished here, one wavefront per row.
+// Partial-writing schedules: after a chunk-first block wrote its partials for
+// rows [rb, rb+nrows), count its arrival on each row; the rows for which it
+// is the last contributor are finished here (Eqn 2 over the row's partials,
+// then O/n) by the whole block at once: each row gets 256/R threads and each
+// thread a slice of d, and all loads of a batch of partials are in flight
+// together. The rows' partial lists are part of the kernel context, so they
+// are requested before the block waits for its own stores; after the
+// arrival only the partials themselves are read (one round trip per batch
+// instead of a chain of index, maximum and vector loads per row).
+constexpr int kFinishBatch = 4;  // partials per batch of the block-wide finish
+
+// The partial list of the row this thread would finish (static context):
+// its range is requested once the block's first K/V loads are out
+// (finish_range) and its first indices right after the chunk loop
+// (finish_ids), so the arrival waits for nothing but the block's own
+// partial stores and no load of the block's start waits behind them.
+struct FinishList {
+  int k0 = 0, k1 = 0;
+  int pid[kFinishBatch] = {-1, -1, -1, -1};
+};
+template <int R>
+__device__ __forceinline__ void finish_range(const KcfParams& P, int rb, int nrows, FinishList& f) {
+  const int i = static_cast<int>(threadIdx.x) / (256 / R);
+  if (P.cnt && i < nrows) {
+    f.k0 = P.part_ptr[rb + i];
+    f.k1 = P.part_ptr[rb + i + 1];
+  }
+}
+__device__ __forceinline__ void finish_ids(const KcfParams& P, FinishList& f) {
+#pragma unroll
+  for (int j = 0; j < kFinishBatch; ++j) f.pid[j] = f.k0 + j < f.k1 ? P.parts[f.k0 + j] : -1;
+}
+
 template <typename T, int D, int R>
 __device__ __forceinline__ void cf_arrive(const KcfParams& P, int rb, int nrows, int h,
-                                          float (*red)[R]) {
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+                                          float (*red)[R], FinishList fl) {
+  constexpr int TPR = 256 / R;   // threads per row
+  constexpr int DPT = D / TPR;   // d values per thread
+  constexpr int NBF = kFinishBatch;
+  static_assert(DPT % 4 == 0 && DPT >= 4, "finish layout");
+  const int tid = threadIdx.x;
+  const int i = tid / TPR, d0 = (tid % TPR) * DPT;
+  const bool mine = i < nrows;
+  const int row = rb + i;
+  const int k0 = fl.k0, k1 = fl.k1;
+  int pid[NBF];
+#pragma unroll
+  for (int j = 0; j < NBF; ++j) pid[j] = fl.pid[j];
   wait_stores();
   __syncthreads();  // every wavefront's partial stores have completed
   unsigned* flags = reinterpret_cast<unsigned*>(&red[0][0]);
   if (tid < R) {
     int last = 0;
     if (tid < nrows) {
-      const int row = rb + tid;
-      last = arrive_last(P.cnt + static_cast<size_t>(row) * P.H + h,
-                         P.part_ptr[row + 1] - P.part_ptr[row]);
+      const int r = rb + tid;
+      last = arrive_last(P.cnt + static_cast<size_t>(r) * P.H + h,
+                         P.part_ptr[r + 1] - P.part_ptr[r]);
     }
     flags[tid] = last;
   }
   __syncthreads();
-  bool any = false;
-  for (int r = w; r < nrows; r += 4) any |= flags[r] != 0;
-  if (!any) return;
-  for (int r = w; r < nrows; r += 4)
-    if (flags[r])
-      finish_row<T, D, true>(P.part_ptr, P.parts, P.ws_o, P.o_bytes, P.ws_ml, P.o, P.row_map, P.H, rb + r,
-                             h, lane);
+  if (!mine || !flags[i]) return;  // no barrier follows
+  compiler_fence();
+  const int H = P.H;
+  const __amdgpu_buffer_rsrc_t rs = part_rsrc(P.ws_o, P.o_bytes);
+  float m = kNegBig, n = 0.f, acc[DPT];
+#pragma unroll
+  for (int e = 0; e < DPT; ++e) acc[e] = 0.f;
+  const int p0 = pid[0];  // a finishing row has at least one partial
+  for (int kb = k0; kb < k1; kb += NBF) {
+    if (kb > k0) {
+#pragma unroll
+      for (int j = 0; j < NBF; ++j) pid[j] = kb + j < k1 ? P.parts[kb + j] : -1;
+    }
+    float pm[NBF], pn[NBF];
+    float4 pv[NBF][DPT / 4];
+#pragma unroll
+    for (int j = 0; j < NBF; ++j) {
+      const int pk = pid[j] >= 0 ? pid[j] : p0;  // absent: read a valid partial, weight 0
+      const float* ml = reinterpret_cast<const float*>(P.ws_ml + static_cast<size_t>(pk) * H + h);
+      pm[j] = ld_dev(ml);
+      pn[j] = ld_dev(ml + 1);
+#pragma unroll
+      for (int q = 0; q < DPT / 4; ++q) pv[j][q] = ld_dev4(rs, part_off(pk, H, D, h, d0 + 4 * q));
+    }
+    float M = m;
+#pragma unroll
+    for (int j = 0; j < NBF; ++j)
+      if (pid[j] >= 0) M = fmaxf(M, pm[j]);
+    const float a = fast_exp2(m - M);
+    n *= a;
+#pragma unroll
+    for (int e = 0; e < DPT; ++e) acc[e] *= a;
+#pragma unroll
+    for (int j = 0; j < NBF; ++j) {
+      const float wj = pid[j] >= 0 ? fast_exp2(pm[j] - M) : 0.f;
+      n = fmaf(wj, pn[j], n);
+#pragma unroll
+      for (int q = 0; q < DPT / 4; ++q) {
+        acc[4 * q] = fmaf(wj, pv[j][q].x, acc[4 * q]);
+        acc[4 * q + 1] = fmaf(wj, pv[j][q].y, acc[4 * q + 1]);
+        acc[4 * q + 2] = fmaf(wj, pv[j][q].z, acc[4 * q + 2]);
+        acc[4 * q + 3] = fmaf(wj, pv[j][q].w, acc[4 * q + 3]);
+      }
+    }
+    m = M;
+  }
+  const float inv = 1.f / n;
+  T* out = static_cast<T*>(P.o) + (static_cast<size_t>(io_row(P.row_map, row)) * H + h) * D + d0;
+#pragma unroll
+  for (int e = 0; e < DPT; ++e) out[e] = static_cast<T>(acc[e] * inv);
 }
 
 // Matrix-core operand layout used below (16x16 output tiles, 64 lanes;
@@ -655,6 +739,7 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
   const int rb = sg.row_begin + z * R;
   const int nrows = min(R, sg.row_end - rb);
   if (nrows <= 0) return;
+  FinishList fl;
   const int nrt = (nrows + 15) / 16;
   const _Float16* q = static_cast<const _Float16*>(P.q);
   const _Float16* kpool = static_cast<const _Float16*>(P.kpool) + h * P.hs;
@@ -724,6 +809,7 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
   const int cm = min(C, 64);
   load_k(slot, 0, cm);
   load_v(slot, 0, cm);
+  finish_range<R>(P, rb, nrows, fl);
   int len = __builtin_amdgcn_readlane(my_len, 0);
   if (len < cm) {  // uniform; rare
     load_k(slot, 0, len);
@@ -814,6 +900,7 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
     len = nlen;
   }
 
+  finish_ids(P, fl);
   // Merge the four wavefront states per row: common max, rescaled sums.
   float nw[NRT];
 #pragma unroll
@@ -913,7 +1000,7 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
       }
     }
   }
-  if (P.cnt) cf_arrive<OUT_T, D, R>(P, rb, nrows, h, reinterpret_cast<float (*)[R]>(mbuf));
+  if (P.cnt) cf_arrive<OUT_T, D, R>(P, rb, nrows, h, reinterpret_cast<float (*)[R]>(mbuf), fl);
 }
 
 // fp32 chunk-first: the same schedule on the 16x16x4 fp32 matrix-core op.
@@ -938,6 +1025,8 @@ __device__ __forceinline__ void kcf_f32_block(const KcfParams& P, int seg, int z
   const int rb = sg.row_begin + z * R;
   const int nrows = min(R, sg.row_end - rb);
   if (nrows <= 0) return;
+  FinishList fl;
+  finish_range<R>(P, rb, nrows, fl);
   const int nrt = (nrows + 15) / 16;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int l16 = lane & 15, g = lane >> 4;
@@ -1042,6 +1131,7 @@ __device__ __forceinline__ void kcf_f32_block(const KcfParams& P, int seg, int z
     }
   }
 
+  finish_ids(P, fl);
 #pragma unroll
   for (int t = 0; t < NRT; ++t) {
     float ns = n_part[t];
@@ -1088,7 +1178,7 @@ __device__ __forceinline__ void kcf_f32_block(const KcfParams& P, int seg, int z
       }
     }
   }
-  if (P.cnt) cf_arrive<OUT_T, D, R>(P, rb, nrows, h, red);
+  if (P.cnt) cf_arrive<OUT_T, D, R>(P, rb, nrows, h, red, fl);
 }
 
 // ---------------------------------------------------------------------------
