@@ -50,6 +50,33 @@ __device__ __forceinline__ float group_sum(float x) {
   return x;
 }
 
+// Reductions over the four 16-lane rows of a wavefront (lanes l, l^16, l^32,
+// l^48) with gfx950's row-swap moves instead of LDS permutes. Swapping a
+// register with a copy of itself, odd rows against even rows, leaves rows
+// 2k and 2k+1 of the value in the two registers of every lane of both rows;
+// the half swap does the same for the two 32-lane halves. The s_nop covers
+// the wait states the swap needs after a vector write of its operands.
+__device__ __forceinline__ void swap_rows16(float& a, float& b) {
+  asm volatile("s_nop 1\n\tv_permlane16_swap_b32 %0, %1" : "+v"(a), "+v"(b));
+}
+__device__ __forceinline__ void swap_halves32(float& a, float& b) {
+  asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1" : "+v"(a), "+v"(b));
+}
+__device__ __forceinline__ float rows4_max(float x) {
+  float a = x, b = x;
+  swap_rows16(a, b);
+  float c = fmaxf(a, b), d = c;
+  swap_halves32(c, d);
+  return fmaxf(c, d);
+}
+__device__ __forceinline__ float rows4_sum(float x) {
+  float a = x, b = x;
+  swap_rows16(a, b);
+  float c = a + b, d = c;
+  swap_halves32(c, d);
+  return c + d;
+}
+
 template <typename T>
 struct Elem;
 template <>

@@ -679,6 +679,9 @@ __device__ __forceinline__ void cf_arrive(const KcfParams& P, int rb, int nrows,
   for (int e = 0; e < DPT; ++e) out[e] = static_cast<T>(acc[e] * inv);
 }
 
+// Lazy reference maximum of the chunk-first softmax (log2 units): P <= 2^8.
+constexpr float kLazyMax = 8.f;
+
 // Matrix-core operand layout used below (16x16 output tiles, 64 lanes;
 // l16 = lane % 16, g = lane / 16):
 //   A (16 x K): lane holds row l16, its K-slice g;   B (K x 16): column l16,
@@ -711,7 +714,7 @@ constexpr int kcf_f16_lds_bytes() {
 //     LDS (row stride d+4 halves: the four lane groups read disjoint banks).
 // No barrier inside the chunk loop; the four wavefront states are merged
 // once at the end of the segment.
-template <int D, int NRT, typename OUT_T = _Float16>
+template <int D, int NRT, typename OUT_T = _Float16, int PF = 1>
 __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z, int h, char* lds) {
   constexpr int KS = D / 32;      // 16x16x32 steps over d for S^T
   constexpr int DT = D / 16;      // 16-wide d tiles of O^T (every wavefront holds all)
@@ -772,27 +775,52 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
 
   // Segment chunks (at most 64): lane j holds chunk j's slot and length.
   const int my_len = lane < sg.n_chunks ? P.slot_len[my_slot] : 0;
-  // Software pipeline without extra registers: the next block's K rows are
-  // requested as soon as this block's S^T MFMAs have read theirs, and its V
-  // rows as soon as this block's V rows are in LDS, so each block's loads
-  // overlap the previous block's softmax and P.V; every iteration issues the
-  // same loads, so each wait covers only the rows it needs.
-  // Unconditional loads: rows past a block's end re-read its last row (valid
-  // and finite); their scores are masked to -inf below, so P = 0.
+  // Software pipeline: block n's K rows are requested as soon as the S^T
+  // MFMAs of block n - PF have read that register set, and its V rows as soon
+  // as block n - PF's V rows are in LDS, so each block's loads overlap the
+  // arithmetic of the PF blocks before it. PF = 1 needs no extra registers
+  // (the fused launch, whose register count sets every block's occupancy);
+  // PF = 2 keeps two register sets (the loop is unrolled by two, so no set is
+  // ever copied while its loads are in flight) and halves the wait per block
+  // of long chunk-first chains when no sequence-first block shares the launch.
+  // Every step issues the same loads, so each wait covers only the rows it
+  // needs. Unconditional loads: rows past a block's end re-read its last row
+  // (valid and finite); their scores are masked to -inf below, so P = 0.
   const int ktok = 16 * w + l16;  // this lane's K row within a block
-  half8 kf[KS];
-  uint4 vr[NVL];
-  auto load_k = [&](int sl, int tb, int ln) {
-    const int ntb = min(64, ln - tb);
-    const _Float16* kb = kpool + sl * slot_stride + static_cast<size_t>(tb) * D;
+  const int nch = sg.n_chunks;
+  struct Cur {
+    int j, t0, slot, len;  // block = rows t0 .. t0 + 63 of the segment's chunk j
+  };
+  auto valid = [&](const Cur& c) { return c.j < nch; };
+  auto step = [&](Cur c) {
+    c.t0 += 64;
+    if (c.t0 >= c.len) {
+      c.t0 = 0;
+      ++c.j;
+      if (c.j < nch) {
+        c.slot = __builtin_amdgcn_readlane(my_slot, c.j);
+        c.len = __builtin_amdgcn_readlane(my_len, c.j);
+      }
+    }
+    return c;
+  };
+  // past the end: re-read one row of block c (every lane the same row: two
+  // cache lines, never used)
+  auto dummy = [&](Cur c) {
+    c.t0 = c.len - 1;
+    return c;
+  };
+  auto load_k = [&](half8 (&kf)[KS], const Cur& c) {
+    const int ntb = min(64, c.len - c.t0);
+    const _Float16* kb = kpool + c.slot * slot_stride + static_cast<size_t>(c.t0) * D;
 #pragma unroll
     for (int s = 0; s < KS; ++s)
       kf[s] = *reinterpret_cast<const half8*>(kb + static_cast<size_t>(min(ktok, ntb - 1)) * D +
                                               32 * s + 8 * g);
   };
-  auto load_v = [&](int sl, int tb, int ln) {
-    const int ntb = min(64, ln - tb);
-    const _Float16* vb = vpool + sl * slot_stride + static_cast<size_t>(tb) * D;
+  auto load_v = [&](uint4 (&vr)[NVL], const Cur& c) {
+    const int ntb = min(64, c.len - c.t0);
+    const _Float16* vb = vpool + c.slot * slot_stride + static_cast<size_t>(c.t0) * D;
 #pragma unroll
     for (int i = 0; i < NVL; ++i) {
       const int tl = lane / GPR + TPL * i;
@@ -800,40 +828,9 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
                                               (lane % GPR) * 8);
     }
   };
-  // The first block's rows go out before the first chunk's length is
-  // known, as if it were full (rows clamped to the tile: in bounds); a
-  // shorter chunk is requested again with the right clamp (rows past its
-  // length may hold anything, even NaN, and are never used).
-  int j = 0, t0 = 0;
-  int slot = __builtin_amdgcn_readlane(my_slot, 0);
-  const int cm = min(C, 64);
-  load_k(slot, 0, cm);
-  load_v(slot, 0, cm);
-  finish_range<R>(P, rb, nrows, fl);
-  int len = __builtin_amdgcn_readlane(my_len, 0);
-  if (len < cm) {  // uniform; rare
-    load_k(slot, 0, len);
-    load_v(slot, 0, len);
-  }
-  while (true) {
-    const int nt = min(64, len - t0);
-    // the block after this one; after the last block, the loads re-read one
-    // row of it (every lane the same row: two cache lines, never used)
-    int nj = j, nt0 = t0 + 64, nslot = slot, nlen = len;
-    if (nt0 >= len) {
-      nt0 = 0;
-      ++nj;
-      if (nj < sg.n_chunks) {
-        nslot = __builtin_amdgcn_readlane(my_slot, nj);
-        nlen = __builtin_amdgcn_readlane(my_len, nj);
-      }
-    }
-    const bool more = nj < sg.n_chunks;
-    if (!more) {
-      nt0 = len - 1;
-      nslot = slot;
-      nlen = len;
-    }
+  // block `cur` from the register set (kf, vr); then block `req` into it
+  auto body = [&](half8 (&kf)[KS], uint4 (&vr)[NVL], const Cur& cur, const Cur& req) {
+    const int nt = min(64, cur.len - cur.t0);
     floatx4 sacc[NRT];
 #pragma unroll
     for (int t = 0; t < NRT; ++t) {
@@ -844,12 +841,21 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
           sacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(kf[s], qf[t][s], sacc[t], 0, 0, 0);
       }
     }
-    load_k(nslot, nt0, nlen);
+    load_k(kf, req);
+    // Online softmax with a lazy reference maximum: a row's reference m_run
+    // moves only when the block's maximum exceeds it by more than kLazyMax
+    // (log2 units), so P = exp2(S - m_run) <= 2^kLazyMax (exactly
+    // representable range of fp16, same relative precision), and the O
+    // accumulators (in AGPRs: a rescale is a read, a multiply and a write
+    // per register) are rescaled only in the blocks where some row's
+    // reference moved (wave-uniform test), not in every block. Any reference
+    // gives the same O / n; the partial carries the reference it used.
     half4 ph[NRT];
     float alpha[NRT];
+    bool moved = false;
 #pragma unroll
     for (int t = 0; t < NRT; ++t) {
-      float lmax = kNegBig;
+      float lmax = -INFINITY;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int tok = 16 * w + 4 * g + i;
@@ -857,10 +863,10 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
         sacc[t][i] = x;
         lmax = fmaxf(lmax, x);
       }
-      lmax = fmaxf(lmax, __shfl_xor(lmax, 16));
-      lmax = fmaxf(lmax, __shfl_xor(lmax, 32));
-      const float mn = fmaxf(m_run[t], lmax);
+      lmax = rows4_max(lmax);
+      const float mn = lmax > m_run[t] + kLazyMax ? lmax : m_run[t];
       alpha[t] = fast_exp2(m_run[t] - mn);
+      moved |= mn != m_run[t];
       m_run[t] = mn;
       float ps = 0.f;
 #pragma unroll
@@ -879,7 +885,13 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
       dst[0] = make_uint2(vr[i].x, vr[i].y);
       dst[1] = make_uint2(vr[i].z, vr[i].w);
     }
-    load_v(nslot, nt0, nlen);
+    load_v(vr, req);
+    if (__any(moved)) {
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int t = 0; t < NRT; ++t) acc[dt][t] *= alpha[t];
+    }
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
       half4 va;
@@ -887,17 +899,51 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
       for (int i = 0; i < 4; ++i) va[i] = vw[(4 * g + i) * RS + 16 * dt + l16];
 #pragma unroll
       for (int t = 0; t < NRT; ++t) {
-        if (t < nrt) {
-          acc[dt][t] *= alpha[t];
-          acc[dt][t] = __builtin_amdgcn_mfma_f32_16x16x16f16(va, ph[t], acc[dt][t], 0, 0, 0);
-        }
+        if (t < nrt) acc[dt][t] = __builtin_amdgcn_mfma_f32_16x16x16f16(va, ph[t], acc[dt][t], 0, 0, 0);
       }
     }
-    if (!more) break;
-    j = nj;
-    t0 = nt0;
-    slot = nslot;
-    len = nlen;
+  };
+  // The first block's rows go out before the first chunk's length is
+  // known, as if it were full (rows clamped to the tile: in bounds); a
+  // shorter chunk is requested again with the right clamp (rows past its
+  // length may hold anything, even NaN, and are never used).
+  const int cm = min(C, 64);
+  Cur cur{0, 0, __builtin_amdgcn_readlane(my_slot, 0), cm};
+  half8 kA[KS];
+  uint4 vA[NVL];
+  load_k(kA, cur);
+  load_v(vA, cur);
+  finish_range<R>(P, rb, nrows, fl);
+  cur.len = __builtin_amdgcn_readlane(my_len, 0);
+  if (cur.len < cm) {  // uniform; rare
+    load_k(kA, cur);
+    load_v(vA, cur);
+  }
+  if constexpr (PF == 1) {
+    while (true) {
+      const Cur nxt = step(cur);
+      const bool more = valid(nxt);
+      body(kA, vA, cur, more ? nxt : dummy(cur));
+      if (!more) break;
+      cur = nxt;
+    }
+  } else {
+    half8 kB[KS];
+    uint4 vB[NVL];
+    Cur q1 = step(cur);
+    load_k(kB, valid(q1) ? q1 : dummy(cur));
+    load_v(vB, valid(q1) ? q1 : dummy(cur));
+    Cur q2 = valid(q1) ? step(q1) : q1;
+    while (true) {
+      body(kA, vA, cur, valid(q2) ? q2 : dummy(cur));  // cur in A; q2 into A
+      if (!valid(q1)) break;
+      const Cur q3 = valid(q2) ? step(q2) : q2;
+      body(kB, vB, q1, valid(q3) ? q3 : dummy(q1));    // q1 in B; q3 into B
+      if (!valid(q2)) break;
+      cur = q2;
+      q1 = q3;
+      q2 = valid(q3) ? step(q3) : q3;
+    }
   }
 
   finish_ids(P, fl);
@@ -1281,6 +1327,18 @@ __global__ __launch_bounds__(256) void kcf_kernel(KcfParams P, int zb) {
     kcf_f32_block<D, NRT>(P, rest / zb, rest % zb, h, lds);
 }
 
+// Chunk-first work alone (no sequence-first item in the call, e.g. identical
+// sequences): 16-row blocks with the two-deep prefetch, which the fused
+// kernel's register budget does not allow.
+template <int D>
+__global__ __launch_bounds__(256) void kcf_deep_kernel(KcfParams P, int zb) {
+  __shared__ __attribute__((aligned(16))) char lds[kcf_f16_lds_bytes<D, 1>()];
+  const int b = static_cast<int>(blockIdx.x);
+  const int h = b % P.H;
+  const int rest = b / P.H;
+  kcf_f16_block<D, 1, _Float16, 2>(P, rest / zb, rest % zb, h, lds);
+}
+
 template <typename T, int D>
 __global__ __launch_bounds__(256) void ksf_kernel(KsfParams P) {
   __shared__ __attribute__((aligned(16))) char lds[ksf_lds_bytes<T, D>()];
@@ -1295,6 +1353,12 @@ hipError_t launch_phases(const TppParams& P, int n_sf, int schedule, int mask, h
   if ((schedule == 1 || schedule == 2) && both) {
     // the fused launch always takes 16-row chunk-first blocks
     if constexpr (NRT == 1) {
+      if constexpr (sizeof(T) == 2) {
+        if (n_sf == 0) {  // chunk-first work alone
+          if (P.n_cf > 0) kcf_deep_kernel<D><<<P.n_cf, 256, 0, s>>>(P.cf, P.zb);
+          return hipSuccess;
+        }
+      }
       const int grid = P.n_cf + n_sf;
       if (grid > 0) tpp_kernel<T, D, NRT><<<grid, 256, 0, s>>>(P);
       return hipSuccess;

@@ -94,33 +94,6 @@ __device__ __forceinline__ void kpf_load_rows(const _Float16* kbase, const _Floa
   }
 }
 
-// Reductions over the four 16-lane rows of a wavefront (lanes l, l^16, l^32,
-// l^48) with gfx950's row-swap moves instead of LDS permutes. Swapping a
-// register with a copy of itself, odd rows against even rows, leaves rows
-// 2k and 2k+1 of the value in the two registers of every lane of both rows;
-// the half swap does the same for the two 32-lane halves. The s_nop covers
-// the wait states the swap needs after a vector write of its operands.
-__device__ __forceinline__ void kpf_swap_rows(float& a, float& b) {
-  asm volatile("s_nop 1\n\tv_permlane16_swap_b32 %0, %1" : "+v"(a), "+v"(b));
-}
-__device__ __forceinline__ void kpf_swap_halves(float& a, float& b) {
-  asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1" : "+v"(a), "+v"(b));
-}
-__device__ __forceinline__ float kpf_rows_max(float x) {
-  float a = x, b = x;
-  kpf_swap_rows(a, b);
-  float c = fmaxf(a, b), d = c;
-  kpf_swap_halves(c, d);
-  return fmaxf(c, d);
-}
-__device__ __forceinline__ float kpf_rows_sum(float x) {
-  float a = x, b = x;
-  kpf_swap_rows(a, b);
-  float c = a + b, d = c;
-  kpf_swap_halves(c, d);
-  return c + d;
-}
-
 template <int D, int TOK>
 constexpr int kpf_tile_bytes() { return TOK * (kpf_k_stride<D>() + kpf_v_stride<D>()) * 2; }
 
@@ -350,7 +323,7 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
       for (int jt = 0; jt < JT; ++jt)
 #pragma unroll
         for (int i = 0; i < 4; ++i) lmax = fmaxf(lmax, sacc[t][jt][i]);
-      lmax = kpf_rows_max(lmax);
+      lmax = rows4_max(lmax);
       // running max in scaled base-2 units; qscale > 0 commutes with max
       const float mn = fmaxf(m_run[t], lmax * P.qscale);
       alpha[t] = fast_exp2(m_run[t] - mn);
@@ -422,7 +395,7 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
   float n_row[QT];
 #pragma unroll
   for (int t = 0; t < QT; ++t) {
-    n_row[t] = kpf_rows_sum(n_part[t]);
+    n_row[t] = rows4_sum(n_part[t]);
   }
   if constexpr (NGRP > 1) {
     // groups 1.. hand their (m, n, O) to group 0 through LDS (Eqn 2)
