@@ -698,7 +698,7 @@ template <int D, int NRT>
 constexpr int kcf_f16_lds_bytes() {
   constexpr int R = 16 * NRT;
   constexpr int vb = 4 * 16 * (D + 4) * 2;  // four wavefront V slices
-  constexpr int ob = R * (D + 4) * 4;       // merge buffer (reuses the slices)
+  constexpr int ob = 4 * R * (D + 4) * 4;   // one merge buffer per wavefront (reuses the slices)
   return (vb > ob ? vb : ob) + 2 * 4 * R * 4;
 }
 
@@ -722,7 +722,7 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
   constexpr int OS = D + 4;       // merge buffer row stride (floats)
   constexpr int R = 16 * NRT;
   constexpr int VB = 4 * 16 * RS * 2;
-  constexpr int OB = R * OS * 4;
+  constexpr int OB = 4 * R * OS * 4;
   constexpr int BIG = VB > OB ? VB : OB;
   constexpr int GPR = D / 8;      // 16-byte granules per token row
   constexpr int TPL = 64 / GPR;   // tokens per wavefront load
@@ -976,26 +976,21 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
     Nrow[t] = N;
     (void)nw[t];
   }
-  for (int ww = 0; ww < 4; ++ww) {
-    if (w == ww) {
+  // every wavefront parks its rescaled O^T in its own buffer ([row][d], one
+  // 16-byte write per tile); the partial stores below add the four
+  {
+    float* mine = obuf + w * (R * OS);
 #pragma unroll
-      for (int t = 0; t < NRT; ++t) {
-        if (t < nrt) {
-          const int r = 16 * t + l16;
+    for (int t = 0; t < NRT; ++t) {
+      if (t < nrt) {
+        const int r = 16 * t + l16;
 #pragma unroll
-          for (int dt = 0; dt < DT; ++dt) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              float* dst = obuf + r * OS + 16 * dt + 4 * g + i;
-              const float v = acc[dt][t][i] * scale[t];
-              *dst = ww == 0 ? v : *dst + v;
-            }
-          }
-        }
+        for (int dt = 0; dt < DT; ++dt)
+          *reinterpret_cast<floatx4*>(mine + r * OS + 16 * dt + 4 * g) = acc[dt][t] * scale[t];
       }
     }
-    __syncthreads();
   }
+  __syncthreads();
   // write the segment's partial (O, m, n) for every covered row
   const size_t pbase = static_cast<size_t>(sg.part_base + (rb - sg.row_begin));
   const bool fold = sg.pad0 != 0;
@@ -1025,6 +1020,11 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
     for (int e = tid; e < nrows * (D / 4); e += 256) {
       const int r = e / (D / 4), d = 4 * (e % (D / 4));
       float4 v = *reinterpret_cast<const float4*>(obuf + r * OS + d);
+#pragma unroll
+      for (int ww = 1; ww < 4; ++ww) {
+        const float4 u = *reinterpret_cast<const float4*>(obuf + ww * (R * OS) + r * OS + d);
+        v = make_float4(v.x + u.x, v.y + u.y, v.z + u.z, v.w + u.w);
+      }
       const uint32_t off = part_off(static_cast<int>(pbase) + r, H, D, h, d);
       if (fold) {
         const float4 pv = ld_dev4(rs, off);
