@@ -694,12 +694,13 @@ constexpr float kLazyMax = 8.f;
 // (as [row][token]) and V is staged in LDS ([token][d], rows padded by two
 // elements so the transposed A-operand reads of four lane groups fall in
 // disjoint banks).
-template <int D, int NRT>
+template <int D, int NRT, int NCH = 1>
 constexpr int kcf_f16_lds_bytes() {
   constexpr int R = 16 * NRT;
-  constexpr int vb = 4 * 16 * (D + 4) * 2;  // four wavefront V slices
-  constexpr int ob = 4 * R * (D + 4) * 4;   // one merge buffer per wavefront (reuses the slices)
-  return (vb > ob ? vb : ob) + 2 * 4 * R * 4;
+  constexpr int NW = 4 * NCH;               // wavefronts
+  constexpr int vb = NW * 16 * (D + 16) * 2;  // one V slice per wavefront
+  constexpr int ob = NW * R * (D + 4) * 4;    // one merge buffer per wavefront (reuses the slices)
+  return (vb > ob ? vb : ob) + 2 * NW * R * 4;
 }
 
 // Chunk-first block, fp16. Wavefronts work independently: wavefront w owns
@@ -711,28 +712,33 @@ constexpr int kcf_f16_lds_bytes() {
 //   O^T += V^T P^T: 16x16x16 MFMA whose B operand (lane holds k = 4g..4g+3
 //     of column l16) is exactly the layout S^T came out in, so P never leaves
 //     the registers; V^T comes from the wavefront's own 16-token V slice in
-//     LDS (row stride d+4 halves: the four lane groups read disjoint banks).
+//     LDS through the transposing ds_read_b64_tr_b16, all d tiles requested
+//     before the first of their MFMAs (row stride d+16 halves: the eight rows
+//     one half-wavefront reads fall in disjoint banks).
 // No barrier inside the chunk loop; the four wavefront states are merged
 // once at the end of the segment.
-template <int D, int NRT, typename OUT_T = _Float16, int PF = 1>
+template <int D, int NRT, typename OUT_T = _Float16, int NCH = 1>
 __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z, int h, char* lds) {
   constexpr int KS = D / 32;      // 16x16x32 steps over d for S^T
   constexpr int DT = D / 16;      // 16-wide d tiles of O^T (every wavefront holds all)
-  constexpr int RS = D + 4;       // V slice row stride (halves)
+  constexpr int RS = D + 16;      // V slice row stride (halves)
   constexpr int OS = D + 4;       // merge buffer row stride (floats)
   constexpr int R = 16 * NRT;
-  constexpr int VB = 4 * 16 * RS * 2;
-  constexpr int OB = 4 * R * OS * 4;
+  constexpr int NW = 4 * NCH;     // wavefronts: NCH chains of four
+  constexpr int VB = NW * 16 * RS * 2;
+  constexpr int OB = NW * R * OS * 4;
   constexpr int BIG = VB > OB ? VB : OB;
   constexpr int GPR = D / 8;      // 16-byte granules per token row
   constexpr int TPL = 64 / GPR;   // tokens per wavefront load
   constexpr int NVL = 16 / TPL;   // V loads per lane per block
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int wq = w & 3;                                       // token quarter of a block
+  const int chain = __builtin_amdgcn_readfirstlane(w >> 2);  // chain (wave-uniform)
   const int l16 = lane & 15, g = lane >> 4;
   _Float16* vw = reinterpret_cast<_Float16*>(lds) + w * 16 * RS;
   float* obuf = reinterpret_cast<float*>(lds);
-  float* mbuf = reinterpret_cast<float*>(lds + BIG);  // [4][R]
-  float* nbuf = mbuf + 4 * R;                         // [4][R]
+  float* mbuf = reinterpret_cast<float*>(lds + BIG);  // [NW][R]
+  float* nbuf = mbuf + NW * R;                        // [NW][R]
 
   // The segment's slots sit at a fixed stride, so they are requested with
   // the segment record, in the same round trip (one per lane).
@@ -775,18 +781,14 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
 
   // Segment chunks (at most 64): lane j holds chunk j's slot and length.
   const int my_len = lane < sg.n_chunks ? P.slot_len[my_slot] : 0;
-  // Software pipeline: block n's K rows are requested as soon as the S^T
-  // MFMAs of block n - PF have read that register set, and its V rows as soon
-  // as block n - PF's V rows are in LDS, so each block's loads overlap the
-  // arithmetic of the PF blocks before it. PF = 1 needs no extra registers
-  // (the fused launch, whose register count sets every block's occupancy);
-  // PF = 2 keeps two register sets (the loop is unrolled by two, so no set is
-  // ever copied while its loads are in flight) and halves the wait per block
-  // of long chunk-first chains when no sequence-first block shares the launch.
-  // Every step issues the same loads, so each wait covers only the rows it
-  // needs. Unconditional loads: rows past a block's end re-read its last row
-  // (valid and finite); their scores are masked to -inf below, so P = 0.
-  const int ktok = 16 * w + l16;  // this lane's K row within a block
+  // Software pipeline: the next block's K rows are requested as soon as the
+  // S^T MFMAs have read this block's, and its V rows as soon as this block's
+  // V rows are in LDS, so each block's loads overlap the previous block's
+  // arithmetic with no extra registers (the fused launch's register count
+  // sets every block's occupancy). Every step issues the same loads, so each
+  // wait covers only the rows it needs; past the last block a chain
+  // re-requests one row of its last block (never used).
+  const int ktok = 16 * wq + l16;  // this lane's K row within a block
   const int nch = sg.n_chunks;
   struct Cur {
     int j, t0, slot, len;  // block = rows t0 .. t0 + 63 of the segment's chunk j
@@ -796,7 +798,7 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
     c.t0 += 64;
     if (c.t0 >= c.len) {
       c.t0 = 0;
-      ++c.j;
+      c.j += NCH;
       if (c.j < nch) {
         c.slot = __builtin_amdgcn_readlane(my_slot, c.j);
         c.len = __builtin_amdgcn_readlane(my_len, c.j);
@@ -804,29 +806,40 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
     }
     return c;
   };
-  // past the end: re-read one row of block c (every lane the same row: two
-  // cache lines, never used)
+  // past the end: one row of block c (the rest of the block reads as zeros)
   auto dummy = [&](Cur c) {
     c.t0 = c.len - 1;
     return c;
   };
+  // K and V rows of block c go through a buffer descriptor that spans
+  // exactly the block's valid rows: its base (slot, first row) is
+  // wave-uniform, so the address arithmetic is scalar and each lane's byte
+  // offset is the same in every block, and rows past the valid length read
+  // as zeros (the descriptor's range check; their scores are masked below,
+  // so they add nothing).
+  auto rows_rsrc = [&](const _Float16* pool, const Cur& c) {
+    const int slot = __builtin_amdgcn_readfirstlane(c.slot);
+    const int t0 = __builtin_amdgcn_readfirstlane(c.t0);
+    const int ntb = min(64, __builtin_amdgcn_readfirstlane(c.len) - t0);
+    return __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<_Float16*>(pool + slot * slot_stride + static_cast<size_t>(t0) * D), 0, ntb * D * 2,
+        kRsrcWord3);
+  };
+  const int ko = (ktok * D + 8 * g) * 2;  // this lane's K granule (s = 0), bytes
+  int vo[NVL];                            // this lane's V granules, bytes
+#pragma unroll
+  for (int i = 0; i < NVL; ++i) vo[i] = ((16 * wq + lane / GPR + TPL * i) * D + (lane % GPR) * 8) * 2;
   auto load_k = [&](half8 (&kf)[KS], const Cur& c) {
-    const int ntb = min(64, c.len - c.t0);
-    const _Float16* kb = kpool + c.slot * slot_stride + static_cast<size_t>(c.t0) * D;
+    const __amdgpu_buffer_rsrc_t r = rows_rsrc(kpool, c);
 #pragma unroll
     for (int s = 0; s < KS; ++s)
-      kf[s] = *reinterpret_cast<const half8*>(kb + static_cast<size_t>(min(ktok, ntb - 1)) * D +
-                                              32 * s + 8 * g);
+      kf[s] = __builtin_bit_cast(half8, __builtin_amdgcn_raw_buffer_load_b128(r, ko + 64 * s, 0, 0));
   };
   auto load_v = [&](uint4 (&vr)[NVL], const Cur& c) {
-    const int ntb = min(64, c.len - c.t0);
-    const _Float16* vb = vpool + c.slot * slot_stride + static_cast<size_t>(c.t0) * D;
+    const __amdgpu_buffer_rsrc_t r = rows_rsrc(vpool, c);
 #pragma unroll
-    for (int i = 0; i < NVL; ++i) {
-      const int tl = lane / GPR + TPL * i;
-      vr[i] = *reinterpret_cast<const uint4*>(vb + static_cast<size_t>(min(16 * w + tl, ntb - 1)) * D +
-                                              (lane % GPR) * 8);
-    }
+    for (int i = 0; i < NVL; ++i)
+      vr[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, vo[i], 0, 0));
   };
   // block `cur` from the register set (kf, vr); then block `req` into it
   auto body = [&](half8 (&kf)[KS], uint4 (&vr)[NVL], const Cur& cur, const Cur& req) {
@@ -858,7 +871,7 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
       float lmax = -INFINITY;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int tok = 16 * w + 4 * g + i;
+        const int tok = 16 * wq + 4 * g + i;
         const float x = tok < nt ? sacc[t][i] * P.qscale : -INFINITY;
         sacc[t][i] = x;
         lmax = fmaxf(lmax, x);
@@ -892,58 +905,44 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
 #pragma unroll
         for (int t = 0; t < NRT; ++t) acc[dt][t] *= alpha[t];
     }
+    half4 va[DT];  // lane: tokens 4g..4g+3 of column 16dt + l16
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) va[dt] = lds_read_tr16(vw + (4 * g + (l16 >> 2)) * RS + 16 * dt + 4 * (l16 & 3));
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
-      half4 va;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) va[i] = vw[(4 * g + i) * RS + 16 * dt + l16];
 #pragma unroll
       for (int t = 0; t < NRT; ++t) {
-        if (t < nrt) acc[dt][t] = __builtin_amdgcn_mfma_f32_16x16x16f16(va, ph[t], acc[dt][t], 0, 0, 0);
+        if (t < nrt) acc[dt][t] = __builtin_amdgcn_mfma_f32_16x16x16f16(va[dt], ph[t], acc[dt][t], 0, 0, 0);
       }
     }
   };
   // The first block's rows go out before the first chunk's length is
-  // known, as if it were full (rows clamped to the tile: in bounds); a
-  // shorter chunk is requested again with the right clamp (rows past its
-  // length may hold anything, even NaN, and are never used).
+  // known, as if it were full (a range over the slot's first min(C, 64)
+  // rows: in bounds, but rows past the length may hold anything, even NaN);
+  // a shorter chunk is requested again with its own range, so those rows
+  // read as zeros. Chain k takes chunks k, k + NCH, ... (a chain with no
+  // chunk skips the loop and merges an empty state).
   const int cm = min(C, 64);
-  Cur cur{0, 0, __builtin_amdgcn_readlane(my_slot, 0), cm};
+  Cur cur{chain, 0, __builtin_amdgcn_readlane(my_slot, chain), cm};
   half8 kA[KS];
   uint4 vA[NVL];
-  load_k(kA, cur);
-  load_v(vA, cur);
-  finish_range<R>(P, rb, nrows, fl);
-  cur.len = __builtin_amdgcn_readlane(my_len, 0);
-  if (cur.len < cm) {  // uniform; rare
+  const bool work = chain < nch;
+  if (work) {
     load_k(kA, cur);
     load_v(vA, cur);
   }
-  if constexpr (PF == 1) {
-    while (true) {
-      const Cur nxt = step(cur);
-      const bool more = valid(nxt);
-      body(kA, vA, cur, more ? nxt : dummy(cur));
-      if (!more) break;
-      cur = nxt;
-    }
-  } else {
-    half8 kB[KS];
-    uint4 vB[NVL];
-    Cur q1 = step(cur);
-    load_k(kB, valid(q1) ? q1 : dummy(cur));
-    load_v(vB, valid(q1) ? q1 : dummy(cur));
-    Cur q2 = valid(q1) ? step(q1) : q1;
-    while (true) {
-      body(kA, vA, cur, valid(q2) ? q2 : dummy(cur));  // cur in A; q2 into A
-      if (!valid(q1)) break;
-      const Cur q3 = valid(q2) ? step(q2) : q2;
-      body(kB, vB, q1, valid(q3) ? q3 : dummy(q1));    // q1 in B; q3 into B
-      if (!valid(q2)) break;
-      cur = q2;
-      q1 = q3;
-      q2 = valid(q3) ? step(q3) : q3;
-    }
+  finish_range<R>(P, rb, nrows, fl);
+  cur.len = __builtin_amdgcn_readlane(my_len, chain);
+  if (work && cur.len < cm) {  // uniform; rare
+    load_k(kA, cur);
+    load_v(vA, cur);
+  }
+  while (work) {
+    const Cur nxt = step(cur);
+    const bool more = valid(nxt);
+    body(kA, vA, cur, more ? nxt : dummy(cur));
+    if (!more) break;
+    cur = nxt;
   }
 
   finish_ids(P, fl);
@@ -967,10 +966,10 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
     const int r = 16 * t + l16;
     float M = kNegBig;
 #pragma unroll
-    for (int ww = 0; ww < 4; ++ww) M = fmaxf(M, mbuf[ww * R + r]);
+    for (int ww = 0; ww < NW; ++ww) M = fmaxf(M, mbuf[ww * R + r]);
     float N = 0.f;
 #pragma unroll
-    for (int ww = 0; ww < 4; ++ww) N += nbuf[ww * R + r] * fast_exp2(mbuf[ww * R + r] - M);
+    for (int ww = 0; ww < NW; ++ww) N += nbuf[ww * R + r] * fast_exp2(mbuf[ww * R + r] - M);
     scale[t] = fast_exp2(m_run[t] - M);
     Mrow[t] = M;
     Nrow[t] = N;
@@ -1017,11 +1016,11 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
   }
   {
     const __amdgpu_buffer_rsrc_t rs = part_rsrc(P.ws_o, P.o_bytes);
-    for (int e = tid; e < nrows * (D / 4); e += 256) {
+    for (int e = tid; e < nrows * (D / 4); e += 256 * NCH) {
       const int r = e / (D / 4), d = 4 * (e % (D / 4));
       float4 v = *reinterpret_cast<const float4*>(obuf + r * OS + d);
 #pragma unroll
-      for (int ww = 1; ww < 4; ++ww) {
+      for (int ww = 1; ww < NW; ++ww) {
         const float4 u = *reinterpret_cast<const float4*>(obuf + ww * (R * OS) + r * OS + d);
         v = make_float4(v.x + u.x, v.y + u.y, v.z + u.z, v.w + u.w);
       }
@@ -1328,15 +1327,19 @@ __global__ __launch_bounds__(256) void kcf_kernel(KcfParams P, int zb) {
 }
 
 // Chunk-first work alone (no sequence-first item in the call, e.g. identical
-// sequences): 16-row blocks with the two-deep prefetch, which the fused
-// kernel's register budget does not allow.
+// sequences): 16-row blocks of eight wavefronts, two chains of four that take
+// alternate chunks of the segment, so each block keeps twice the loads in
+// flight and the chains' states are merged once at the end. Measured on
+// Table 3's all-shared cells against one chain with a two-deep prefetch
+// (same) and four chains (slower: more fixed cost per chain).
+constexpr int kDeepChains = 2;
 template <int D>
-__global__ __launch_bounds__(256) void kcf_deep_kernel(KcfParams P, int zb) {
-  __shared__ __attribute__((aligned(16))) char lds[kcf_f16_lds_bytes<D, 1>()];
+__global__ __launch_bounds__(256 * kDeepChains) void kcf_deep_kernel(KcfParams P, int zb) {
+  __shared__ __attribute__((aligned(16))) char lds[kcf_f16_lds_bytes<D, 1, kDeepChains>()];
   const int b = static_cast<int>(blockIdx.x);
   const int h = b % P.H;
   const int rest = b / P.H;
-  kcf_f16_block<D, 1, _Float16, 2>(P, rest / zb, rest % zb, h, lds);
+  kcf_f16_block<D, 1, _Float16, kDeepChains>(P, rest / zb, rest % zb, h, lds);
 }
 
 template <typename T, int D>
@@ -1355,7 +1358,7 @@ hipError_t launch_phases(const TppParams& P, int n_sf, int schedule, int mask, h
     if constexpr (NRT == 1) {
       if constexpr (sizeof(T) == 2) {
         if (n_sf == 0) {  // chunk-first work alone
-          if (P.n_cf > 0) kcf_deep_kernel<D><<<P.n_cf, 256, 0, s>>>(P.cf, P.zb);
+          if (P.n_cf > 0) kcf_deep_kernel<D><<<P.n_cf, 256 * kDeepChains, 0, s>>>(P.cf, P.zb);
           return hipSuccess;
         }
       }

@@ -349,6 +349,31 @@ def test_edge_cases(dtype):
     assert_close(o, p.reference(rs, qq, 0.37), dtype, "scale 0.37")
 
 
+@pytest.mark.parametrize("c,d", [(64, 128), (128, 128), (32, 64)])
+def test_chunk_first_only_calls(c, d):
+    """Identical prompts, so every chunk is shared and the call is chunk-first
+    work alone (its own launch, several chains of chunks per block), with
+    segments of 1, 2, 3 and 5 chunks and the automatic length (chains with
+    no chunk, uneven chains), 20 rows (a second row block of 4 rows) and a
+    partial last chunk."""
+    print(f"[case] chunk-first-only calls c={c} d={d}", flush=True)
+    rng = np.random.default_rng(31 + c + d)
+    H, n, rows = 4, 700, 20
+    p = Pair(c, H, d, np.float16, 64)
+    k, v = _kv(rng, n, H, d, np.float16)
+    for sid in range(rows):
+        p.insert(sid, np.arange(n), k, v)
+    qmap = {sid: rng.standard_normal((H, d)).astype(np.float16) for sid in range(rows)}
+    ref = None
+    for sched in (2, 1):
+        for seg in (1, 2, 3, 5, -1):
+            p.cache.set_tuning(seg_chunks=seg, schedule=sched)
+            o, qq, rs = p.attention(qmap)
+            if ref is None:
+                ref = p.reference(rs, qq, 0.0)
+            assert_close(o, ref, np.float16, f"chunk-first only c={c} d={d} schedule={sched} seg={seg}")
+
+
 def test_workspace_is_checked():
     rng = np.random.default_rng(2)
     p = _small_pair()
