@@ -152,15 +152,16 @@ void build_work(const ChunkTree& tree, const Tables& T, int32_t seg_chunks, int3
   // sequence-first stream (the private K/V at ~6 TB/s) is long enough to hide
   // a longer chain at ~3 us per chunk under load; longer segments mean fewer
   // partials per row. When the sequence-first blocks take more than one
-  // round of the chip's resident slots (four blocks per compute unit), a
-  // chain is also at most twice as long as the longest row's private chunk
-  // list: longer chains outlast the sequence-first blocks and finish the
-  // rows late (measured on a tree of 64 rows with 4 private chunks each:
-  // 57.0 us with 8-chunk segments against 60.6 us for 16). With one round
-  // or less the chains are the critical path whatever their length, and
-  // fewer partials win (32 rows decoding from a 4096-token prompt with 1 to
-  // 200 private tokens: 16-chunk segments 23-32 us, 2-8-chunk segments
-  // 26-43 us).
+  // round of the chip's resident slots (four blocks per compute unit) and
+  // stream at least 4 chunks each, a chain is also at most twice as long as
+  // the longest row's private chunk list: longer chains outlast the
+  // sequence-first blocks and finish the rows late (measured on a tree of
+  // 64 rows with 4 private chunks each: 57.0 us with 8-chunk segments
+  // against 60.6 us for 16). Otherwise the chains are the critical path
+  // whatever their length and fewer partials win (32 rows decoding from a
+  // 4096-token prompt with 1 to 200 private tokens: 16-chunk segments 23-32
+  // us, 2-8-chunk segments 26-43 us; 96 rows over a 2048-token prompt with
+  // one private chunk: 40 us against 55 us with 2-chunk segments).
   if (seg_chunks <= 0) {
     int64_t work = 0;
     for (const auto& chain : runs) {
@@ -175,7 +176,7 @@ void build_work(const ChunkTree& tree, const Tables& T, int32_t seg_chunks, int3
     const double ksf_us = static_cast<double>(priv_tokens) * num_heads * token_head_bytes / 6.0e6;
     int64_t cap = std::min<int64_t>(64, std::max<int64_t>(16, static_cast<int64_t>(ksf_us / 3.0)));
     const int64_t cus = num_cus > 0 ? num_cus : 256;
-    if (max_priv > 0 && B * num_heads > 4 * cus) cap = std::min<int64_t>(cap, 2 * max_priv);
+    if (max_priv >= 4 && B * num_heads > 4 * cus) cap = std::min<int64_t>(cap, 2 * max_priv);
     seg_chunks = static_cast<int32_t>(std::min<int64_t>(cap, std::max<int64_t>(1, (work + cus - 1) / cus)));
   }
   if (seg_chunks > 64) seg_chunks = 64;  // the chunk-first kernel keeps a segment's slots in lanes

@@ -165,6 +165,9 @@ def decode_run(b, n_s, n_c, checkpoints, seed):
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         cache.append(ids, toks[step], k, v)
+        # the step's context (tables, work lists, their upload) is built here,
+        # outside the attention time and inside the library-step time
+        cache.prepare()
         a = torch.cuda.Event(enable_timing=True)
         e = torch.cuda.Event(enable_timing=True)
         a.record()
