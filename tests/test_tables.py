@@ -377,6 +377,48 @@ def test_partial_free_workspace_is_one_accumulator_per_row():
     B.ca_destroy(h)
 
 
+def _auto_segment(c, H, seqs):
+    h = B.ca_create(c, H, 128, B.CA_FP16, 1 << 14)
+    for sid, toks in enumerate(seqs):
+        B.ca_insert(h, sid, toks)
+    B.ca_workspace_size(h)  # builds the work lists
+    seg = B.ca_stats(h)["seg_chunks"]
+    B.ca_destroy(h)
+    return seg
+
+
+def _prompt_plus_one(rows, n_shared):
+    return [list(range(n_shared)) + [1_000_000 + r] for r in range(rows)]
+
+
+@pytest.mark.parametrize("case,want", [
+    ("config2", 4),          # quota 16 chunks x 2 row blocks x 32 heads / 256 CUs = 4
+    ("config3", 16),         # quota 16
+    ("config4", 8),          # quota 16, capped at twice the 4 private chunks (2,048 blocks)
+    ("b32_p4096_u1", 16),    # quota 16; one round of blocks: no private cap
+    ("b96_p2048_u1", 16),    # quota 24 -> 32, base cap 16; one private chunk: no private cap
+    ("b48_p2048_u1", 16),    # quota 12 -> 16
+    ("b48_p1024_u1", 8),     # quota 6 -> 8
+])
+def test_automatic_segment_length(case, want):
+    """The automatic chunk-first segment length: about one block per compute
+    unit (256 on MI355X), rounded up to a power of two, at most 16 chunks
+    unless the private stream is long enough to hide longer chains, and at
+    most twice the longest private chunk list when the sequence-first blocks
+    take more than one round of resident slots and stream at least 4 chunks
+    each."""
+    _lib_or_skip()
+    if case.startswith("config"):
+        wl = make_static(int(case[-1]))
+        seqs = [s.tokens(wl.segments) for s in wl.seqs]
+        c, H = wl.c, wl.H
+    else:
+        rows, n_shared = {"b32_p4096_u1": (32, 4096), "b96_p2048_u1": (96, 2048),
+                          "b48_p2048_u1": (48, 2048), "b48_p1024_u1": (48, 1024)}[case]
+        seqs, c, H = _prompt_plus_one(rows, n_shared), 64, 32
+    assert _auto_segment(c, H, seqs) == want
+
+
 def test_prepare_on_a_table_only_cache():
     """ca_prepare builds the host context only (nothing to upload)."""
     _lib_or_skip()
