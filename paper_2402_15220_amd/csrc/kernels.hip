@@ -688,12 +688,6 @@ constexpr float kLazyMax = 8.f;
 //   K-slice g;   C/D (16 x 16): lane holds rows 4g..4g+3 of column l16.
 // Both operands use the same K-slice per lane, so the contraction does not
 // depend on how the hardware orders K inside a slice.
-//
-// Wavefront w owns tokens 16w..16w+15 of each 64-token block for S^T and the
-// d columns [w*D/4, (w+1)*D/4) for O^T. P = exp2(S - m) travels through LDS
-// (as [row][token]) and V is staged in LDS ([token][d], rows padded by two
-// elements so the transposed A-operand reads of four lane groups fall in
-// disjoint banks).
 template <int D, int NRT, int NCH = 1>
 constexpr int kcf_f16_lds_bytes() {
   constexpr int R = 16 * NRT;
@@ -1048,8 +1042,12 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
   if (P.cnt) cf_arrive<OUT_T, D, R>(P, rb, nrows, h, reinterpret_cast<float (*)[R]>(mbuf), fl);
 }
 
-// fp32 chunk-first: the same schedule on the 16x16x4 fp32 matrix-core op.
-// Operands are single floats (A: row l16, k = g; B: column l16, k = g).
+// fp32 chunk-first on the 16x16x4 fp32 matrix-core op (operands are single
+// floats: A row l16, k = g; B column l16, k = g), with the earlier schedule:
+// wavefront w computes S^T for tokens 16w..16w+15 of each 64-token block and
+// O^T for the d columns [w*D/4, (w+1)*D/4), so P = exp2(S - m) goes through
+// LDS ([row][token]) and V is staged in LDS ([token][d], rows padded by one
+// element), with barriers inside the chunk loop.
 template <int D, int NRT>
 constexpr int kcf_f32_lds_bytes() {
   return 64 * (D + 1) * 4 + 16 * NRT * (64 + 1) * 4 + 4 * 16 * NRT * 4;
