@@ -1,6 +1,6 @@
 """The paper's microkernel experiments, re-run on one MI355X with synthetic data.
 
-    python -m paper_2402_15220_amd.sweeps [table3] [fig3] [fig4] [reduce]
+    python -m paper_2402_15220_amd.sweeps [table3] [fig3] [fig4] [reduce] [allshared]
 
 Workload of the experiments section (microkernel evaluation): batch mode, b
 sequences whose n_p prompt tokens start with n_s shared tokens, h=32 heads,
@@ -18,6 +18,8 @@ d=128, chunk c=64, fp16.
           attention) on the host clock.
   fig4    the same decode for n_c=64 tokens, n_s in 1024 and 2048, b from 16
           to 96 (Figure 4's batch sweep).
+  allshared  Table 3's n_s = n_p cells alone (identical prompts: chunk-first
+          work only), e.g. to collect counters for that kernel.
   reduce  the two ways of reducing partials (Section 3.3, further
           optimizations) on the static trees (one prompt of 1024 or 4096
           tokens shared by 32 rows; a two-level tree of 64 rows): segmented
@@ -117,9 +119,9 @@ def _cold_median(fn, flush, n):
     return float(np.median([a.elapsed_time(b) * 1e3 for a, b in evs]))
 
 
-def table3(flush, b=32, warm_calls=100, cold_calls=20):
+def table3(flush, b=32, warm_calls=100, cold_calls=20, shared_fracs=(0, 2, 3, 4)):
     for n_p in (1024, 2048, 4096):
-        for n_s in (0, n_p // 2, 3 * n_p // 4, n_p):
+        for n_s in (n_p * f // 4 for f in shared_fracs):
             cache, g = build_batch(b, n_p, n_s, seed=7000 + n_p + n_s)
             q = torch.randn((b, H, D), generator=g, device="cuda", dtype=torch.float16)
             o = torch.empty_like(q)
@@ -261,7 +263,8 @@ def main(argv=None):
     flush = torch.ones(1 << 29, dtype=torch.float16, device="cuda")  # 1 GiB
     for w in args.which:
         {"table3": lambda: table3(flush), "fig3": fig3, "fig4": fig4,
-         "reduce": lambda: reduce_sweep(flush)}[w]()
+         "reduce": lambda: reduce_sweep(flush),
+         "allshared": lambda: table3(flush, shared_fracs=(4,))}[w]()
 
 
 if __name__ == "__main__":
