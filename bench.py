@@ -180,7 +180,7 @@ def main():
     del cache, q, o
     torch.cuda.empty_cache()
     if not args.no_other_configs and args.config == 2:
-        out["other_configs"] = {str(c): other_config(c, args.steps, not args.no_cold) for c in (3, 4)}
+        out["other_configs"] = {str(c): other_config(c, args.steps, not args.no_cold) for c in (1, 3, 4)}
     if not args.no_dynamic:
         out["dynamic"] = dynamic_run()
     if not args.no_prefill:
@@ -202,7 +202,8 @@ def static_setup(config, seg=0, split=-1, schedule=-1):
 
     wl = make_static(config)
     nodes = sum(-(-len(s) // wl.c) for s in wl.segments)
-    cache = Cache(wl.c, wl.H, wl.d, nodes + 16, dtype=torch.float16)
+    tdt = torch.float32 if np.dtype(wl.dtype) == np.float32 else torch.float16
+    cache = Cache(wl.c, wl.H, wl.d, nodes + 16, dtype=tdt)
     seg_dev = [(torch.from_numpy(s.k).cuda(), torch.from_numpy(s.v).cuda()) for s in wl.segments]
     for s in wl.seqs:
         cache.insert(s.seq_id, s.tokens(wl.segments), torch.cat([seg_dev[i][0] for i in s.segs]),
@@ -212,7 +213,7 @@ def static_setup(config, seg=0, split=-1, schedule=-1):
     rows = cache.seq_order()
     q = torch.from_numpy(np.ascontiguousarray(wl.q[rows])).cuda()
     o = torch.empty_like(q)
-    model = call_model(cache.tables(), wl.H, wl.d, 2)
+    model = call_model(cache.tables(), wl.H, wl.d, np.dtype(wl.dtype).itemsize)
     torch.cuda.synchronize()
     return wl, cache, q, o, rows, model
 
@@ -580,6 +581,7 @@ def cpu_baseline(wl, rows, seconds, with_dynamic=True):
         _oracle_rows(t, rows, q, wl.scale, range(len(rows)), pool, 1)
         single_s = time.perf_counter() - t0
         dyn = dynamic_oracle_sample(pool, threads) if with_dynamic else None
+    c1 = config1_oracle()
     out = {"value": n * len(rows) / el, "unit": "tok/s", "cores": threads, "kind": "oracle",
            "sample": f"{n} full calls of the workload (B={len(rows)} rows x {wl.H} heads, float64 "
                      f"NumPy, rows split over {threads} threads), after one untimed call",
@@ -587,10 +589,39 @@ def cpu_baseline(wl, rows, seconds, with_dynamic=True):
            "host_cpus": len(os.sched_getaffinity(0)),
            "single_thread": {"ms_per_call": single_s * 1e3, "tok_per_s": len(rows) / single_s},
            "tree_ops": {"what": f"building the bench tree: {len(wl.seqs)} inserts with K/V rows",
-                        "ms": tree_build_s * 1e3}}
+                        "ms": tree_build_s * 1e3},
+           "config1_single_thread": c1}
     if dyn is not None:
         out["dynamic"] = dyn
     return out
+
+
+def config1_oracle(repeats=20):
+    """The oracle on the tiny fp32 tree (4 rows of a 128-token prompt plus 32
+    unique tokens, 2 heads, d=64), single-threaded: tree build and the call's
+    attention (median of `repeats`)."""
+    import numpy as np
+
+    from oracle import OracleTree
+    from workloads import make_static
+
+    wl = make_static(1)
+    t = OracleTree(c=wl.c)
+    t0 = time.perf_counter()
+    for s in wl.seqs:
+        k, v = s.kv(wl.segments)
+        t.insert(s.seq_id, s.tokens(wl.segments), k, v)
+    build_ms = (time.perf_counter() - t0) * 1e3
+    rows = [s.seq_id for s in wl.seqs]
+    q = wl.q[rows]
+    ts = []
+    for _ in range(repeats):
+        t0 = time.perf_counter()
+        _oracle_rows(t, rows, q, wl.scale, range(len(rows)), None, 1)
+        ts.append(time.perf_counter() - t0)
+    ms = float(np.median(ts)) * 1e3
+    return {"workload": wl.name, "tree_build_ms": build_ms, "ms_per_call": ms,
+            "tok_per_s": len(rows) / (ms * 1e-3)}
 
 
 def dynamic_oracle_sample(pool, threads, sample_steps=(0, 16)):
