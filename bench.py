@@ -175,7 +175,7 @@ def main():
         cache.set_tuning(phase_mask=2)    # the sequence-first kernel alone, same flush
         ksf_cold = cold_times(call, model["ksf_bytes"], model["B"])
         cache.set_tuning(phase_mask=7)
-        out["sequence_first_alone"]["cold"] = {k: ksf_cold[k] for k in ("us_per_call", "GBps", "frac")}
+        out["sequence_first_alone"]["cold"] = {k: ksf_cold[k] for k in ("us_per_call", "GBps", "frac", "stream")}
     cache.close()
     del cache, q, o
     torch.cuda.empty_cache()
@@ -323,13 +323,34 @@ def cold_times(call, nbytes, rows, n=30):
         evs.append((a, b))
     torch.cuda.synchronize()
     us = float(np.median([a.elapsed_time(b) * 1e3 for a, b in evs]))
+    # The same cold calls without a marker pair around each: n (flush, call)
+    # pairs back to back, less n flushes alone, both between one event pair
+    # (the device time a cold call adds to a stream, its launch gap included)
+    def span(with_call):
+        torch.cuda.synchronize()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(n):
+            flush.sum()
+            if with_call:
+                call()
+        b.record()
+        b.synchronize()
+        return a.elapsed_time(b) * 1e3
+    diffs = [(span(True) - span(False)) / n for _ in range(3)]
+    us_diff = float(np.median(diffs))
     from paper_2402_15220_amd.roofline import PEAK_HBM_GBPS
 
     gbps = nbytes / (us * 1e-6) / 1e9
     return {"us_per_call": us, "tok_per_s": rows / (us * 1e-6), "GBps": gbps,
             "frac": gbps / PEAK_HBM_GBPS, "calls": n,
             "flush": "clean 1 GiB read between calls; median of per-call event pairs "
-                     "(each pair adds ~2 us of marker overhead)"}
+                     "(each pair adds ~2 us of marker overhead)",
+            "stream": {"us_per_call": us_diff,
+                       "frac": nbytes / (us_diff * 1e-6) / 1e9 / PEAK_HBM_GBPS,
+                       "how": f"{n} (flush, call) pairs back to back less {n} flushes alone, "
+                              "one event pair around each sequence; median of 3"}}
 
 
 def prefill_run(n=100):
