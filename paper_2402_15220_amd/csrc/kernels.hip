@@ -940,14 +940,12 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
   }
 
   finish_ids(P, fl);
-  // Merge the four wavefront states per row: common max, rescaled sums.
-  float nw[NRT];
+  // Merge the wavefront states per row: common max, rescaled sums.
 #pragma unroll
   for (int t = 0; t < NRT; ++t) {
     float ns = n_part[t];
     ns += __shfl_xor(ns, 16);
     ns += __shfl_xor(ns, 32);
-    nw[t] = ns;
     if (g == 0) {
       mbuf[w * R + 16 * t + l16] = m_run[t];
       nbuf[w * R + 16 * t + l16] = ns;
@@ -967,10 +965,9 @@ __device__ __forceinline__ void kcf_f16_block(const KcfParams& P, int seg, int z
     scale[t] = fast_exp2(m_run[t] - M);
     Mrow[t] = M;
     Nrow[t] = N;
-    (void)nw[t];
   }
   // every wavefront parks its rescaled O^T in its own buffer ([row][d], one
-  // 16-byte write per tile); the partial stores below add the four
+  // 16-byte write per tile); the partial stores below add them up
   {
     float* mine = obuf + w * (R * OS);
 #pragma unroll
