@@ -41,6 +41,24 @@ def _both(p, qmap, label):
     return row_seq
 
 
+def test_noalloc_chunk_first_only_call():
+    """Identical prompts: the call is chunk-first work alone (its own launch),
+    here with its partials and counters in the device scratch."""
+    print("[case] noalloc entry point, chunk-first work only", flush=True)
+    rng = np.random.default_rng(23)
+    H, d, n, rows = 4, 128, 700, 20
+    p = Pair(64, H, d, np.float16, 64)
+    k = rng.standard_normal((n, H, d)).astype(np.float16)
+    v = rng.standard_normal((n, H, d)).astype(np.float16)
+    for sid in range(rows):
+        p.insert(sid, np.arange(n), k, v)
+    qmap = {sid: rng.standard_normal((H, d)).astype(np.float16) for sid in range(rows)}
+    for seg in (-1, 3):
+        p.cache.set_tuning(seg_chunks=seg, schedule=2)
+        p.cache.prepare()
+        _both(p, qmap, f"chunk-first only seg={seg}")
+
+
 def test_noalloc_matches_attention_two_calls_second_smaller():
     print("[case] noalloc entry point on the single-prompt tree", flush=True)
     wl = make_static(2)
