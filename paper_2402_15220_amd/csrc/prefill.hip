@@ -181,8 +181,21 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
   if (v >= n_qt * H * S) return;
   const int tix = v / S, part = v % S;   // the parts of a tile are neighbours (same XCD)
   const int h = tix / n_qt;
-  const int L = chunk_end(P.n_chunks - 1);
   const int q0 = (tix % n_qt) * 64;                            // first query of the tile
+  // this lane's query row of tile t and its q fragments, requested before
+  // anything waits for the chunk table, so the two round trips overlap (and
+  // the first unit's loads overlap q's)
+  int qi[QT];
+  half8 qf[QT][KS];
+#pragma unroll
+  for (int t = 0; t < QT; ++t) {
+    qi[t] = q0 + 16 * (QT * w + t) + l16;
+    const int qr = min(qi[t], n_q - 1);  // rows past n_q load a valid row (never written)
+#pragma unroll
+    for (int s = 0; s < KS; ++s)
+      qf[t][s] = *reinterpret_cast<const half8*>(P.q + (static_cast<size_t>(qr) * H + h) * D + 32 * s + 8 * g);
+  }
+  const int L = chunk_end(P.n_chunks - 1);
   const int pos_last = L - n_q + min(q0 + 63, n_q - 1);        // last position of the tile
   const int pos_first = L - n_q + q0;                          // first position of the tile
   const size_t slot_stride = static_cast<size_t>(P.ss);
@@ -190,25 +203,10 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
   const _Float16* vbase = P.vpool + h * P.hs;
   const int upc = (P.C + TOK - 1) / TOK;                       // units per chunk
 
-  // this lane's query row of tile t, and its position
-  int qi[QT], pos[QT];
-  half8 qf[QT][KS];
+  // this lane's query positions
+  int pos[QT];
 #pragma unroll
-  for (int t = 0; t < QT; ++t) {
-    qi[t] = q0 + 16 * (QT * w + t) + l16;
-    pos[t] = L - n_q + qi[t];
-#pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      if (qi[t] < n_q)
-        qf[t][s] = *reinterpret_cast<const half8*>(P.q + (static_cast<size_t>(qi[t]) * H + h) * D +
-                                                   32 * s + 8 * g);
-      else
-        qf[t][s] = half8{};
-    }
-  }
-  // q has arrived before any chunk load is issued, so the MFMAs inside the
-  // loop never wait on vector memory (the next unit's loads stay in flight)
-  wait_stores();
+  for (int t = 0; t < QT; ++t) pos[t] = L - n_q + qi[t];
   float m_run[QT], n_part[QT];
   floatx4 acc[QT][DT];
 #pragma unroll
