@@ -13,7 +13,10 @@ import os
 
 import numpy as np
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "_lib", "libchunkattn.so")
+# The library built in-tree; CA_LIBRARY names another build of the same
+# sources (for example one with host-side sanitizers).
+LIB_PATH = os.environ.get("CA_LIBRARY") or os.path.join(
+    os.path.dirname(os.path.abspath(__file__)), "_lib", "libchunkattn.so")
 
 CA_OK = 0
 CA_ERR_INVALID = -1

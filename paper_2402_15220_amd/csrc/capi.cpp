@@ -402,8 +402,14 @@ ca_status ca_create(const ca_config* cfg, ca_cache** out) try {
   if (cfg->num_heads < 1) return fail(CA_ERR_INVALID, "ca_create: num_heads < 1");
   if (cfg->head_dim != 64 && cfg->head_dim != 128)
     return fail(CA_ERR_INVALID, "ca_create: head_dim must be 64 or 128");
-  if (cfg->dtype != CA_FP16 && cfg->dtype != CA_FP32)
-    return fail(CA_ERR_INVALID, "ca_create: bad dtype");
+  {
+    // read as its integer representation: a value outside the enumeration is
+    // rejected without being loaded as a ca_dtype
+    int32_t dt;
+    static_assert(sizeof(cfg->dtype) == sizeof(dt), "ca_dtype is a 32-bit enumeration");
+    std::memcpy(&dt, &cfg->dtype, sizeof dt);
+    if (dt != CA_FP16 && dt != CA_FP32) return fail(CA_ERR_INVALID, "ca_create: bad dtype");
+  }
   if (cfg->num_slots < 1 || cfg->num_slots > INT32_MAX)
     return fail(CA_ERR_INVALID, "ca_create: num_slots out of range");
   if ((cfg->k_pool == nullptr) != (cfg->v_pool == nullptr))
