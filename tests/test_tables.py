@@ -458,3 +458,122 @@ def test_host_allocation_failure_is_a_status():
     assert r.returncode == 0, r.stderr[-2000:]
     assert f"status {B.CA_ERR_HOST}" in r.stdout, r.stdout + r.stderr[-2000:]
     assert "out of host memory" in r.stdout
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_random_calls_with_invalid_arguments(seed):
+    """Valid and invalid calls mixed at random through the C ABI: every call
+    returns the status the oracle (or the documented argument rules) gives,
+    a refused call changes nothing observable, and an accepted one leaves the
+    tables equal to the oracle's. Invalid kinds: duplicate and unknown ids,
+    empty and negative tokens, repeated ids in a batch, null arrays with a
+    positive count, a seq_order buffer that is too small, and pool
+    exhaustion."""
+    import ctypes
+    lib = _lib_or_skip()
+    rng = np.random.default_rng(7000 + seed)
+    c = 1 + seed % 4
+    slots = 8 + seed % 5
+    h = B.ca_create(c, 1, 64, B.CA_FP16, slots)
+    t = OracleTree(c=c, num_slots=slots, with_kv=False)
+    live = set()
+    next_sid = 0
+    ora_err = {KeyError: None, ValueError: B.CA_ERR_INVALID, PoolExhausted: B.CA_ERR_NOMEM}
+
+    def toks(n):
+        return rng.integers(0, 3, n).astype(np.int32)
+
+    def lib_status(fn):
+        try:
+            fn()
+            return B.CA_OK
+        except B.ChunkAttnError as e:
+            return e.status
+
+    def ora_status(fn, key_status):
+        try:
+            fn()
+            return B.CA_OK
+        except PoolExhausted:
+            return B.CA_ERR_NOMEM
+        except KeyError:
+            return key_status
+        except ValueError:
+            return ora_err[ValueError]
+
+    m = ctypes.c_int64()
+    for _ in range(70):
+        before = B.ca_export_tables(h)
+        used = B.ca_stats(h)["slots_used"]
+        kind = int(rng.integers(0, 12))
+        ids = sorted(live)
+        if kind == 0 or (kind in (1, 4, 6, 8) and not ids):
+            sid, tk = next_sid, toks(int(rng.integers(1, 3 * c + 4)))
+            want = ora_status(lambda: t.insert(sid, tk), B.CA_ERR_EXISTS)
+            got = lib_status(lambda: B.ca_insert(h, sid, tk))
+            if want == B.CA_OK:
+                live.add(sid)
+                next_sid += 1
+        elif kind == 1:                                     # duplicate id
+            sid = int(rng.choice(ids))
+            want, got = B.CA_ERR_EXISTS, lib_status(lambda: B.ca_insert(h, sid, toks(2)))
+        elif kind == 2:                                     # empty or negative tokens
+            bad = np.zeros(0, np.int32) if rng.integers(0, 2) else np.array([1, -3], np.int32)
+            want, got = B.CA_ERR_INVALID, lib_status(lambda: B.ca_insert(h, next_sid, bad))
+        elif kind == 3:                                     # null array with n > 0
+            fn = [lambda: lib.ca_insert(h, next_sid, None, 3, None, None, None, None),
+                  lambda: lib.ca_extend(h, next_sid, None, 1, None, None, None, None),
+                  lambda: lib.ca_match(h, None, 2, ctypes.byref(m)),
+                  lambda: lib.ca_append_batch(h, 1, None, None, None, None, None)][int(rng.integers(0, 4))]
+            want, got = B.CA_ERR_INVALID, fn()
+        elif kind == 4:                                     # extend a live sequence
+            sid, tk = int(rng.choice(ids)), toks(int(rng.integers(1, 2 * c + 2)))
+            want = ora_status(lambda: t.extend(sid, tk), B.CA_ERR_NOT_FOUND)
+            got = lib_status(lambda: B.ca_extend(h, sid, tk))
+        elif kind == 5:                                     # unknown id
+            fn = [lambda: B.ca_extend(h, 10_000, toks(1)), lambda: B.ca_remove(h, 10_000),
+                  lambda: B.ca_append_batch(h, ids[:1] + [10_000], toks(len(ids[:1]) + 1))]
+            want, got = B.CA_ERR_NOT_FOUND, lib_status(fn[int(rng.integers(0, 3))])
+        elif kind == 6:                                     # batch append
+            sel = [int(s) for s in rng.permutation(ids)[:int(rng.integers(1, len(ids) + 1))]]
+            tk = toks(len(sel))
+            want = ora_status(lambda: t.append_batch(sel, tk), B.CA_ERR_NOT_FOUND)
+            got = lib_status(lambda: B.ca_append_batch(h, sel, tk))
+        elif kind == 7:                                     # an id twice in a batch
+            if not ids:
+                continue
+            sid = int(rng.choice(ids))
+            want, got = B.CA_ERR_INVALID, lib_status(lambda: B.ca_append_batch(h, [sid, sid], toks(2)))
+        elif kind == 8:                                     # remove a live sequence
+            sid = int(rng.choice(ids))
+            want = ora_status(lambda: t.remove(sid), B.CA_ERR_NOT_FOUND)
+            got = lib_status(lambda: B.ca_remove(h, sid))
+            if want == B.CA_OK:
+                live.discard(sid)
+        elif kind == 9:                                     # seq_order buffer too small
+            n = B.ca_num_seqs(h)
+            if n == 0:
+                continue
+            buf = np.zeros(n, np.int64)
+            want = B.CA_ERR_INVALID
+            got = lib.ca_seq_order(h, buf.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), n - 1)
+        elif kind == 10:                                    # prefix lookup, valid or empty
+            tk = toks(int(rng.integers(0, 2 * c + 3)))
+            got = lib.ca_match(h, tk.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), tk.shape[0],
+                               ctypes.byref(m))
+            want = B.CA_OK if tk.shape[0] > 0 else B.CA_ERR_INVALID
+            if got == B.CA_OK:
+                assert m.value == t.match(tk)
+        else:                                               # null output pointers
+            fn = [lambda: lib.ca_num_seqs(h, None), lambda: lib.ca_workspace_size(h, None),
+                  lambda: lib.ca_export_tables(h, None)][int(rng.integers(0, 3))]
+            want, got = B.CA_ERR_INVALID, fn()
+        assert got == want, (kind, got, want)
+        if got != B.CA_OK:
+            after = B.ca_export_tables(h)
+            for k in before:
+                assert np.array_equal(before[k], after[k]), (kind, k)
+            assert B.ca_stats(h)["slots_used"] == used
+        t.check_invariants()
+        _same(B.ca_export_tables(h), tables(t))
+    B.ca_destroy(h)
