@@ -33,6 +33,10 @@ def test_table_tests_under_asan_and_ubsan(tmp_path):
     if runtime is None or shutil.which(libbuild.HIPCC) is None and not os.path.exists(libbuild.HIPCC):
         pytest.skip("no clang ASan runtime or hipcc in this image")
     lib = libbuild.build(sanitize=True, lib=str(tmp_path / "libchunkattn_san.so"))
+    # the build really carries both sanitizers (their runtime entry points are
+    # referenced by the instrumented host code)
+    syms = subprocess.run(["nm", "-D", "--undefined-only", lib], capture_output=True, text=True).stdout
+    assert "__asan_report_load" in syms and "__ubsan_handle_" in syms, syms[:2000]
     env = dict(os.environ)
     env.update(CA_LIBRARY=lib, LD_PRELOAD=runtime,
                # Python's own allocations are not instrumented; leak reports
