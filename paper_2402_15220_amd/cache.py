@@ -181,7 +181,12 @@ class Cache:
         return out
 
     def close(self):
+        """Destroy the library cache. ca_destroy frees the library's device
+        buffers without waiting, so the device is synchronised first (the
+        calls may have been enqueued on several streams)."""
         if self.h is not None:
+            if not self.table_only:
+                torch.cuda.synchronize(self._dev_index)
             B.ca_destroy(self.h)
             self.h = None
 
