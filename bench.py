@@ -127,7 +127,7 @@ def main():
     torch.cuda.synchronize()
 
     tpp_bytes = model["shared_kv"] + model["private_kv"] + model["q"]
-    traffic, traffic_source = counter_traffic(wl.name)
+    traffic, traffic_source = counter_traffic(wl.name, cache.layout)
     tpp_gbps = tpp_bytes / (tpp_us * 1e-6) / 1e9
     ksf_gbps = model["ksf_bytes"] / (ksf_us * 1e-6) / 1e9
     kcf_tflops = model["kcf_flops"] / (kcf_us * 1e-6) / 1e12
@@ -146,6 +146,7 @@ def main():
         "dtype": "f16",
         "data": "synthetic",
         "config": {"workload": wl.name, "B": B, "H": wl.H, "d": wl.d, "c": wl.c,
+                   "pool_layout": cache.layout,
                    "shared_tokens": int(model["shared_kv"] // (2 * wl.H * wl.d * 2)),
                    "private_tokens_per_row": int(model["private_kv"] // (2 * wl.H * wl.d * 2) // B)},
         "value_kind": "warm: back-to-back calls on one resident tree (its 285.7 MB partly stays in "
@@ -282,12 +283,13 @@ def decode_sources_hash(csrc):
     return h.hexdigest()[:16]
 
 
-def counter_traffic(workload):
+def counter_traffic(workload, layout):
     """HBM bytes per tpp_kernel launch, taken from the committed rocprofv3
     counter passes (FETCH_SIZE and WRITE_SIZE, each scaled by what it reads
     for a plain copy of known size); not measured in this run. Returns
     (bytes or None, source): None when the kernels' code changed since the
-    counters were taken (hash mismatch) or the workload differs."""
+    counters were taken (hash mismatch), or the workload or pool layout
+    differs."""
     rel = os.path.join("profiles", "tpp_kernel_single_prompt_b32_traffic.json")
     csrc = os.path.join(ROOT, "paper_2402_15220_amd", "csrc")
     sha = decode_sources_hash(csrc)
@@ -299,8 +301,8 @@ def counter_traffic(workload):
         return None, dict(src, status="no counter record")
     if rec.get("decode_sources_sha256_16") != sha:
         return None, dict(src, status="stale: kernels changed since the counters were taken")
-    if rec.get("workload") != workload:
-        return None, dict(src, status="counters are for another workload")
+    if rec.get("workload") != workload or rec.get("pool_layout") != layout:
+        return None, dict(src, status="counters are for another workload or pool layout")
     return rec["kernels"]["tpp_kernel"]["traffic_bytes"], dict(src, status="current")
 
 

@@ -19,19 +19,23 @@ class Cache:
     """A prefix-tree chunked KV cache on one GPU (or table-only on the host).
 
     Pools are allocated here with torch and lent to the library; q/o rows
-    follow ``seq_order()``. ``layout="split"`` (default) uses two buffers
-    [slot][head][c][d]; ``"interleaved"`` keeps each chunk-head's K and V
-    tiles adjacent in one buffer [slot][head][K|V][c][d] (strided pools).
+    follow ``seq_order()``. ``layout="interleaved"`` (default) keeps each
+    chunk-head's K and V tiles adjacent in one buffer [slot][head][K|V][c][d]
+    (strided pools: a block that reads a chunk's K and then its V reads one
+    contiguous region, which measured faster than two separate regions on
+    every decode workload, most on calls that miss the caches); ``"split"``
+    uses two buffers [slot][head][c][d] (the C ABI's dense default).
     ``k_pool``/``v_pool`` are [slot][head][c][d] views either way.
     """
 
     def __init__(self, chunk_size: int, num_heads: int, head_dim: int, num_slots: int,
                  dtype=torch.float16, device="cuda", table_only: bool = False,
-                 layout: str = "split"):
+                 layout: str = "interleaved"):
         self.c, self.H, self.d = chunk_size, num_heads, head_dim
         self.dtype = dtype
         self.num_slots = num_slots
         self.table_only = table_only
+        self.layout = None if table_only else layout
         if table_only:
             self.k_pool = self.v_pool = None
             self.h = B.ca_create(chunk_size, num_heads, head_dim, _DT[dtype], num_slots)
