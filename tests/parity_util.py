@@ -52,9 +52,10 @@ def assert_close(o, ref, dtype, what=""):
 
 
 class Pair:
-    """The same cache on both sides: the HIP library and the oracle."""
+    """The same cache on both sides: the HIP library and the oracle. Pools
+    are the wrapper's default (K|V-interleaved) unless a layout is named."""
 
-    def __init__(self, c, H, d, dtype, num_slots, oracle_kv=True, layout="split"):
+    def __init__(self, c, H, d, dtype, num_slots, oracle_kv=True, layout="interleaved"):
         self.dtype = np.dtype(dtype)
         self.cache = Cache(c, H, d, num_slots, dtype=TORCH_DT[self.dtype], layout=layout)
         self.tree = OracleTree(c=c, with_kv=oracle_kv)

@@ -24,7 +24,7 @@ def _gpu():
     yield
 
 
-def _static_pair(wl, slack=16, layout="split"):
+def _static_pair(wl, slack=16, layout="interleaved"):
     nodes = sum(-(-len(s) // wl.c) for s in wl.segments)  # aligned configs: one chunk set per segment
     p = Pair(wl.c, wl.H, wl.d, wl.dtype, nodes + slack, layout=layout)
     seg_dev = [(to_dev(s.k), to_dev(s.v)) for s in wl.segments]
@@ -38,9 +38,10 @@ def _static_pair(wl, slack=16, layout="split"):
 
 
 @pytest.mark.parametrize("cfg,layout", [(1, "split"), (2, "split"), (3, "split"), (4, "split"),
-                                        (1, "interleaved"), (2, "interleaved")])
+                                        (1, "interleaved"), (2, "interleaved"), (3, "interleaved"),
+                                        (4, "interleaved")])
 def test_static_config(cfg, layout):
-    """Full-size static trees; K/V pools split (default) and interleaved."""
+    """Full-size static trees; K/V pools split and interleaved (the default)."""
     wl = make_static(cfg)
     print(f"[case] {wl.name} layout={layout}", flush=True)
     p = _static_pair(wl, layout=layout)
