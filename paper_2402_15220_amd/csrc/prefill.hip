@@ -76,27 +76,6 @@ constexpr int kpf_k_stride() { return D + 8; }
 template <int D>
 constexpr int kpf_v_stride() { return D + 16; }
 
-// TOK rows of a chunk's K and V (rows r0 .. r0 + TOK - 1) for a group of GT
-// threads: granule e = tid + GT*u is row r0 + e / (D/8), 16-byte column
-// e % (D/8) (coalesced rows). Rows past the chunk's length re-read its last
-// row (their scores are masked).
-template <int D, int GT, int TOK>
-__device__ __forceinline__ void kpf_load_rows(const _Float16* kbase, const _Float16* vbase,
-                                              size_t slot_stride, int slot, int r0, int len, int tid,
-                                              u32x4 (&kr)[TOK * D / 8 / GT],
-                                              u32x4 (&vr)[TOK * D / 8 / GT]) {
-  constexpr int NG = D / 8;
-  const _Float16* kb = kbase + slot * slot_stride;
-  const _Float16* vb = vbase + slot * slot_stride;
-#pragma unroll
-  for (int u = 0; u < TOK * NG / GT; ++u) {
-    const int e = tid + GT * u;
-    const size_t off = static_cast<size_t>(min(r0 + e / NG, len - 1)) * D + (e % NG) * 8;
-    kr[u] = *reinterpret_cast<const u32x4*>(kb + off);
-    vr[u] = *reinterpret_cast<const u32x4*>(vb + off);
-  }
-}
-
 template <int D, int TOK>
 constexpr int kpf_tile_bytes() { return TOK * (kpf_k_stride<D>() + kpf_v_stride<D>()) * 2; }
 
@@ -253,11 +232,34 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
   // same loads, so the wait before each LDS write covers exactly the
   // registers it needs on every path.
   u32x4 kr[GPT], vr[GPT];
+  // K and V rows of a unit go through buffer descriptors that span exactly
+  // the unit's valid rows: the base (slot, first row) is wave-uniform, so
+  // the address arithmetic is scalar and each lane's byte offset is the same
+  // in every step (granule e = gtid + GT*u2 is row e / (D/8), 16-byte column
+  // e % (D/8): coalesced rows); rows past the chunk's length read as zeros
+  // (their scores are masked, and zero V rows add nothing). 0.9 us less on a
+  // 512-token join than per-lane addresses clamped to the chunk.
+  int goff[GPT];
+#pragma unroll
+  for (int u2 = 0; u2 < GPT; ++u2) {
+    const int e = gtid + GT * u2;
+    goff[u2] = ((e / NG) * D + (e % NG) * 8) * 2;
+  }
   auto issue = [&](int u) {
     int j, r0;
     unit_pos(min(u, u_hi - 1), j, r0);
-    kpf_load_rows<D, GT, TOK>(kbase, vbase, slot_stride, chunk_slot(j), r0,
-                              chunk_end(j) - chunk_start(j), gtid, kr, vr);
+    const int slot = __builtin_amdgcn_readfirstlane(chunk_slot(j));
+    const int rows = min(TOK, chunk_end(j) - chunk_start(j) - r0);
+    const size_t base = static_cast<size_t>(slot) * slot_stride + static_cast<size_t>(r0) * D;
+    const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<_Float16*>(kbase + base), 0, rows * D * 2, kRsrcWord3);
+    const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<_Float16*>(vbase + base), 0, rows * D * 2, kRsrcWord3);
+#pragma unroll
+    for (int u2 = 0; u2 < GPT; ++u2) {
+      kr[u2] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rk, goff[u2], 0, 0));
+      vr[u2] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rv, goff[u2], 0, 0));
+    }
   };
   auto stage = [&](int b) {
     _Float16* k_lds = tile_k(b);
