@@ -50,7 +50,7 @@ __device__ __forceinline__ float group_sum(float x) {
   return x;
 }
 
-// Reductions over the four 16-lane rows of a wavefront (lanes l, l^16, l^32,
+// Maximum over the four 16-lane rows of a wavefront (lanes l, l^16, l^32,
 // l^48) with gfx950's row-swap moves instead of LDS permutes. Swapping a
 // register with a copy of itself, odd rows against even rows, leaves rows
 // 2k and 2k+1 of the value in the two registers of every lane of both rows;
@@ -68,13 +68,6 @@ __device__ __forceinline__ float rows4_max(float x) {
   float c = fmaxf(a, b), d = c;
   swap_halves32(c, d);
   return fmaxf(c, d);
-}
-__device__ __forceinline__ float rows4_sum(float x) {
-  float a = x, b = x;
-  swap_rows16(a, b);
-  float c = a + b, d = c;
-  swap_halves32(c, d);
-  return c + d;
 }
 
 template <typename T>
