@@ -253,7 +253,9 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
     int j, r0;
     unit_pos(min(u, u_hi - 1), j, r0);
     const int slot = __builtin_amdgcn_readfirstlane(chunk_slot(j));
-    const int rows = min(TOK, chunk_end(j) - chunk_start(j) - r0);
+    // a unit past a short chunk's end (chunks longer than TOK count
+    // ceil(c / TOK) units each) gets an empty range: its loads read zeros
+    const int rows = max(0, min(TOK, chunk_end(j) - chunk_start(j) - r0));
     const size_t base = static_cast<size_t>(slot) * slot_stride + static_cast<size_t>(r0) * D;
     const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<_Float16*>(kbase + base), 0, rows * D * 2, kRsrcWord3);
