@@ -255,7 +255,12 @@ __global__ __launch_bounds__(64 * WPG * NGRP) void kpf_kernel(KpfParams P,
     const int slot = __builtin_amdgcn_readfirstlane(chunk_slot(j));
     // a unit past a short chunk's end (chunks longer than TOK count
     // ceil(c / TOK) units each) gets an empty range: its loads read zeros
-    const int rows = max(0, min(TOK, chunk_end(j) - chunk_start(j) - r0));
+    // max(m, 0) written as a scalar instruction: as plain code the compiler
+    // turns the clamp into a vector median-of-three, and the descriptor built
+    // from a vector register then costs a per-lane loop around every load
+    const int m = min(TOK, chunk_end(j) - chunk_start(j) - r0);
+    int rows;
+    asm("s_max_i32 %0, %1, 0" : "=s"(rows) : "s"(m));
     const size_t base = static_cast<size_t>(slot) * slot_stride + static_cast<size_t>(r0) * D;
     const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<_Float16*>(kbase + base), 0, rows * D * 2, kRsrcWord3);
